@@ -1,0 +1,146 @@
+/*
+ * sparselnr.h -- C ABI of the MI355X (gfx950) fused SDDMM->SpMM library.
+ *
+ * Computes, for a sparse matrix B in CSR form and dense C, D, E,
+ *
+ *     A(i,l) = sum_{j,k} B(i,j) * C(i,k) * D(j,k) * E(j,l)
+ *
+ * the <SDDMM, SpMM> computation of Dias et al., "SparseLNR: Accelerating
+ * Sparse Tensor Computations Using Loop Nest Restructuring" (ICS 2022),
+ * Section 3.1 and Figure 2.  The fused entry point runs the paper's
+ * loop-fused, kernel-distributed schedule (Figure 2d; Section 3.1.3): one
+ * pass over the rows of B in which, for every nonzero, a scalar SDDMM value
+ * is produced and immediately consumed by the SpMM update of the row, so no
+ * nnz-sized intermediate exists (Section 4.2: the temporary of this
+ * expression is a scalar because no index below the nest boundary is shared
+ * by producer and consumer).  The unfused entry points are the paper's
+ * separate-kernel schedule (Figures 2a and 2b, Section 3.1.2), kept as the
+ * in-library comparison.
+ *
+ * Layouts (all row-major, densely packed, fp32 values, int32 indices):
+ *   rowptr  int32[N+1]   CSR row offsets; rowptr[0] = 0, non-decreasing
+ *   colidx  int32[nnz]   column of every nonzero, 0 <= colidx[p] < M
+ *   vals    float[nnz]   value of every nonzero
+ *   C       float[N*K]   C(i,k) at C[i*K + k]
+ *   D       float[M*K]   D(j,k) at D[j*K + k]
+ *   E       float[M*L]   E(j,l) at E[j*L + l]
+ *   A       float[N*L]   A(i,l) at A[i*L + l]   (output, overwritten)
+ *   Y       float[nnz]   SDDMM values with the structure of B (unfused only)
+ * where nnz = rowptr[N] (read on the device; never passed in).
+ *
+ * Conventions shared by every compute entry point:
+ *   - All array pointers are DEVICE pointers owned by the caller; the library
+ *     never frees or retains them.  The base pointers must be 4-byte aligned;
+ *     16-byte alignment with K and L multiples of 4 enables the fast paths.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the null
+ *     stream).  No call synchronises with the host.
+ *   - Columns within a row may be unsorted and may repeat (repeats add).
+ *     Preconditions on the CSR arrays are not checked on the device; use
+ *     sparselnr_validate_csr in tests.  nnz and N + nnz must be < 2^31.
+ *   - N = 0 or L = 0 is a no-op.  K = 0 makes every SDDMM value zero.  Rows
+ *     without nonzeros produce zero rows of A.
+ *   - rowptr must be non-NULL when N > 0.  colidx and vals (Y for SpMM) must
+ *     be non-NULL when N > 0; pass any valid device address when nnz = 0.
+ *     C must be non-NULL when N > 0 and K > 0; D when N, M, K > 0; E when
+ *     N, M, L > 0; A when N > 0 and L > 0; Y (unfused/SDDMM) when N > 0.
+ *   - Argument errors are reported BEFORE any HIP call, with no side effect.
+ *   - The fused, unfused and SpMM calls use a workspace of a few MB per
+ *     (device, stream) for rows whose nonzeros are split between workers; it
+ *     is allocated on first use, reused, and freed by sparselnr_release().
+ *     Calls on different streams use different workspaces; calls on one
+ *     stream are ordered by the stream.
+ *   - Results are deterministic: the same inputs give bit-identical outputs
+ *     on the same device model (no floating-point atomics).
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef SPARSELNR_H
+#define SPARSELNR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every int-valued entry point. */
+enum sparselnr_status_code {
+  SPARSELNR_OK = 0,
+  SPARSELNR_ERR_INVALID_ARG = 1, /* NULL pointer, negative size, misuse      */
+  SPARSELNR_ERR_UNSUPPORTED = 2, /* K or L above SPARSELNR_MAX_WIDTH, or
+                                    sizes beyond the int32 index range        */
+  SPARSELNR_ERR_HIP = 3,         /* a HIP call failed; see last_hip_error      */
+  SPARSELNR_ERR_NO_MEMORY = 4,   /* workspace allocation failed               */
+  SPARSELNR_ERR_INVALID_CSR = 5  /* sparselnr_validate_csr found a violation  */
+};
+
+/* Largest accepted K and L. */
+#define SPARSELNR_MAX_WIDTH 65536
+
+/* Version of this interface (incremented on incompatible change). */
+int sparselnr_abi_version(void);
+
+/*
+ * Fused SDDMM->SpMM (Figure 2d; Section 3.1.3):
+ *   A(i,:) = sum_{p in row i} vals[p] * dot(C(i,:), D(colidx[p],:)) * E(colidx[p],:)
+ * A is overwritten.  Arithmetic is fp32 (fused multiply-add), with the
+ * k-reduction done as a lane-parallel tree and the l-update accumulated in
+ * nonzero order.  Needs the per-(device, stream) workspace.
+ */
+int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+                               const float *vals, const float *C,
+                               const float *D, const float *E, float *A,
+                               int64_t N, int64_t M, int64_t K, int64_t L,
+                               void *stream);
+
+/*
+ * Unfused comparison (Figure 2a then Figure 2b, Section 3.1.2): the SDDMM
+ * writes Y (nnz floats, structure of B, same order as colidx), then the SpMM
+ * reads it.  Same result as the fused call up to rounding order.
+ */
+int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+                                 const float *vals, const float *C,
+                                 const float *D, const float *E, float *Y,
+                                 float *A, int64_t N, int64_t M, int64_t K,
+                                 int64_t L, void *stream);
+
+/* SDDMM alone (Figure 2a): Y[p] = vals[p] * dot(C(i,:), D(colidx[p],:)). */
+int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx,
+                    const float *vals, const float *C, const float *D,
+                    float *Y, int64_t N, int64_t M, int64_t K, void *stream);
+
+/* SpMM alone (Figure 2b): A(i,:) = sum_{p in row i} Y[p] * E(colidx[p],:).
+ * A is overwritten.  Needs the per-(device, stream) workspace. */
+int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
+                   const float *Y, const float *E, float *A, int64_t N,
+                   int64_t M, int64_t L, void *stream);
+
+/*
+ * Checks the CSR preconditions on the device: rowptr[0] == 0, rowptr
+ * non-decreasing, 0 <= rowptr[N] <= colidx_len, N + rowptr[N] < 2^31, every
+ * colidx in [0, M).  colidx_len is the number of int32 entries the caller
+ * allocated for colidx; at most that many are read.  SYNCHRONOUS (waits for
+ * `stream`); meant for tests and debugging, not the hot path.  Writes
+ * nnz = rowptr[N] to *nnz_out (host pointer, may be NULL).
+ * Returns SPARSELNR_OK or SPARSELNR_ERR_INVALID_CSR (or an error code).
+ */
+int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx,
+                           int64_t N, int64_t M, int64_t colidx_len,
+                           int64_t *nnz_out, void *stream);
+
+/* Static text for a status code (never NULL). */
+const char *sparselnr_status_string(int status);
+
+/* hipError_t of the last failing HIP call made by this library on the
+ * calling thread (0 if none). */
+int sparselnr_last_hip_error(void);
+
+/* Waits for the device(s) and frees every workspace the library allocated.
+ * Safe to call at any time; later calls allocate again. */
+int sparselnr_release(void);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* SPARSELNR_H */

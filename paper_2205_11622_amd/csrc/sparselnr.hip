@@ -1,0 +1,409 @@
+// Host side of the fused SDDMM->SpMM library: argument checks, variant
+// choice, workspace management and launches.  The C ABI is declared in
+// include/sparselnr.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdlib>
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "sparselnr.h"
+#include "walker.hpp"
+
+namespace {
+
+using slnr::WalkArgs;
+
+thread_local int g_last_hip_error = 0;
+
+constexpr int kBlock = 256;       // threads per block (4 waves)
+constexpr int kMinChunk = 32;     // smallest merge-path slice per worker
+constexpr int kXcds = 8;          // MI355X deals blocks over 8 XCDs
+constexpr int kGenericLT = 4;     // generic path: 4 x 64 = 256 columns per tile
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return SPARSELNR_ERR_HIP;
+}
+
+struct Workspace {
+  void *ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_mu;
+std::map<int, int> g_cus;                                    // device -> CUs
+std::map<std::pair<int, uintptr_t>, int> g_occupancy;        // (device, kernel) -> blocks/CU
+int g_grid_factor = 0;                                       // resident grids per launch
+std::map<std::pair<int, uintptr_t>, Workspace> g_workspace;  // (device, stream)
+
+int current_device(int *dev) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e);
+  return SPARSELNR_OK;
+}
+
+int device_cus(int dev, int *cus) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_cus.find(dev);
+  if (it != g_cus.end()) {
+    *cus = it->second;
+    return SPARSELNR_OK;
+  }
+  int n = 0;
+  hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_fail(e);
+  if (n <= 0) n = 1;
+  g_cus[dev] = n;
+  *cus = n;
+  return SPARSELNR_OK;
+}
+
+// Workspace of at least `bytes` for (device, stream); grows by reallocation
+// after the stream has drained (only on the first calls of a new shape).
+int get_workspace(int dev, hipStream_t stream, size_t bytes, void **out) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  Workspace &w = g_workspace[{dev, (uintptr_t)stream}];
+  if (w.bytes < bytes) {
+    if (w.ptr) {
+      hipError_t e = hipStreamSynchronize(stream);
+      if (e != hipSuccess) return hip_fail(e);
+      e = hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    void *p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) {
+      g_last_hip_error = (int)e;
+      (void)hipGetLastError();
+      return SPARSELNR_ERR_NO_MEMORY;
+    }
+    w.ptr = p;
+    w.bytes = bytes;
+  }
+  *out = w.ptr;
+  return SPARSELNR_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ----------------------------------------------------------- variants
+
+enum Mode { kFused = slnr::kFused, kSddmm = slnr::kSddmm, kSpmm = slnr::kSpmm };
+
+using KernelFn = void (*)(WalkArgs);
+
+struct Variant {
+  KernelFn fn = nullptr;
+  int W = 64;          // lanes per worker
+  bool generic = true; // generic kernel (l-tiles of 256 columns)
+};
+
+template <int MODE, int W, int NB, int KV, int LV, int U>
+Variant fast() {
+  Variant v;
+  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, U>;
+  v.W = W;
+  v.generic = false;
+  return v;
+}
+
+template <int MODE>
+Variant generic() {
+  Variant v;
+  v.fn = slnr::walk_generic<MODE, kGenericLT>;
+  v.W = 64;
+  v.generic = true;
+  return v;
+}
+
+// Fast variants exist for the widths of the benchmark workloads: K = L in
+// {32, 64, 128, 256} (one 16-byte slice of C/D and of E/A per lane) and the
+// asymmetric K = 16, L = 256 (4-lane dot products, 16 per producer pass).
+Variant pick_fused(int64_t K, int64_t L, bool al) {
+  if (al) {
+    if (K == 32 && L == 32) return fast<kFused, 8, 1, 4, 4, 4>();
+    if (K == 64 && L == 64) return fast<kFused, 16, 1, 4, 4, 4>();
+    if (K == 128 && L == 128) return fast<kFused, 32, 1, 4, 4, 4>();
+    if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, 4>();
+    if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, 16>();
+  }
+  return generic<kFused>();
+}
+
+Variant pick_sddmm(int64_t K, bool al) {
+  if (al) {
+    if (K == 16) return fast<kSddmm, 64, 16, 4, 4, 16>();
+    if (K == 32) return fast<kSddmm, 8, 1, 4, 4, 4>();
+    if (K == 64) return fast<kSddmm, 16, 1, 4, 4, 4>();
+    if (K == 128) return fast<kSddmm, 32, 1, 4, 4, 4>();
+    if (K == 256) return fast<kSddmm, 64, 1, 4, 4, 4>();
+  }
+  return generic<kSddmm>();
+}
+
+Variant pick_spmm(int64_t L, bool al) {
+  if (al) {
+    if (L == 32) return fast<kSpmm, 8, 1, 4, 4, 4>();
+    if (L == 64) return fast<kSpmm, 16, 1, 4, 4, 4>();
+    if (L == 128) return fast<kSpmm, 32, 1, 4, 4, 4>();
+    if (L == 256) return fast<kSpmm, 64, 1, 4, 4, 4>();
+  }
+  return generic<kSpmm>();
+}
+
+struct Grid {
+  int blocks;
+  int workers;
+  int xcd_span;
+};
+
+// Resident blocks per CU for `fn` (occupancy query, cached per device).
+int blocks_per_cu(int dev, KernelFn fn, int *out) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (g_grid_factor == 0) {
+    const char *env = getenv("SPARSELNR_GRID_FACTOR");
+    const int f = env ? atoi(env) : 1;
+    g_grid_factor = f >= 1 && f <= 64 ? f : 1;
+  }
+  auto key = std::make_pair(dev, (uintptr_t)fn);
+  auto it = g_occupancy.find(key);
+  if (it != g_occupancy.end()) {
+    *out = it->second;
+    return SPARSELNR_OK;
+  }
+  int nb = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)fn, kBlock, 0);
+  if (e != hipSuccess) return hip_fail(e);
+  if (nb <= 0) nb = 1;
+  g_occupancy[key] = nb;
+  *out = nb;
+  return SPARSELNR_OK;
+}
+
+// One resident grid (times SPARSELNR_GRID_FACTOR): every worker starts at
+// once and owns an equal merge-path slice.
+Grid make_grid(int cus, int per_cu, int W) {
+  Grid g;
+  int blocks = cus * per_cu * g_grid_factor;
+  blocks = ((blocks + kXcds - 1) / kXcds) * kXcds;
+  g.blocks = blocks;
+  g.workers = blocks * (kBlock / 64) * (64 / W);
+  g.xcd_span = blocks / kXcds;
+  return g;
+}
+
+// Runs one merge-path walk (+ carry fixup unless SDDMM) over the whole matrix.
+int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
+  int dev = 0, cus = 0, rc;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
+  int per_cu = 1;
+  if ((rc = blocks_per_cu(dev, v.fn, &per_cu)) != SPARSELNR_OK) return rc;
+  const Grid g = make_grid(cus, per_cu, v.W);
+  a.workers = g.workers;
+  a.min_chunk = kMinChunk;
+  a.xcd_span = g.xcd_span;
+  a.xcds = kXcds;
+  const int64_t tiles = v.generic ? (a.L + 64 * kGenericLT - 1) / (64 * kGenericLT) : 1;
+  const int64_t tile_w = v.generic ? 64 * kGenericLT : a.L;
+  if (mode != kSddmm) {
+    const size_t carry_bytes = (size_t)g.workers * 2 * (size_t)tile_w * sizeof(float);
+    const size_t meta_bytes = (size_t)g.workers * 2 * sizeof(int32_t);
+    void *ws = nullptr;
+    if ((rc = get_workspace(dev, stream, carry_bytes + meta_bytes, &ws)) != SPARSELNR_OK)
+      return rc;
+    a.carry = (float *)ws;
+    a.meta = (int32_t *)((char *)ws + carry_bytes);
+  } else {
+    a.carry = nullptr;
+    a.meta = nullptr;
+  }
+  for (int64_t t = 0; t < (mode == kSddmm ? 1 : tiles); ++t) {
+    a.l0 = (int32_t)(t * tile_w);
+    a.Lw = (int32_t)((a.L - a.l0) < tile_w ? (a.L - a.l0) : tile_w);
+    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(kBlock), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e);
+    if (mode != kSddmm) {
+      const int fix_blocks = (g.workers + (kBlock / 64) - 1) / (kBlock / 64);
+      hipLaunchKernelGGL(slnr::carry_fixup, dim3(fix_blocks), dim3(kBlock), 0, stream,
+                         (const float *)a.carry, (const int32_t *)a.meta, a.out, a.workers,
+                         a.Lw, a.L, a.l0);
+      e = hipGetLastError();
+      if (e != hipSuccess) return hip_fail(e);
+    }
+  }
+  return SPARSELNR_OK;
+}
+
+bool bad_size(int64_t N, int64_t M, int64_t K, int64_t L) {
+  return N < 0 || M < 0 || K < 0 || L < 0;
+}
+
+int check_range(int64_t N, int64_t M, int64_t K, int64_t L) {
+  if (K > SPARSELNR_MAX_WIDTH || L > SPARSELNR_MAX_WIDTH) return SPARSELNR_ERR_UNSUPPORTED;
+  if (N >= ((int64_t)1 << 31) - 1 || M >= ((int64_t)1 << 31)) return SPARSELNR_ERR_UNSUPPORTED;
+  return SPARSELNR_OK;
+}
+
+WalkArgs base_args(const int32_t *rowptr, const int32_t *colidx, const float *vals,
+                   int64_t N, int64_t K, int64_t L) {
+  WalkArgs a{};
+  a.rowptr = rowptr;
+  a.colidx = colidx;
+  a.vals = vals;
+  a.N = N;
+  a.K = (int32_t)K;
+  a.L = (int32_t)L;
+  a.l0 = 0;
+  a.Lw = (int32_t)L;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sparselnr_abi_version(void) { return 1; }
+
+const char *sparselnr_status_string(int status) {
+  switch (status) {
+    case SPARSELNR_OK: return "ok";
+    case SPARSELNR_ERR_INVALID_ARG: return "invalid argument";
+    case SPARSELNR_ERR_UNSUPPORTED: return "unsupported size";
+    case SPARSELNR_ERR_HIP: return "HIP call failed";
+    case SPARSELNR_ERR_NO_MEMORY: return "workspace allocation failed";
+    case SPARSELNR_ERR_INVALID_CSR: return "CSR preconditions violated";
+    default: return "unknown status";
+  }
+}
+
+int sparselnr_last_hip_error(void) { return g_last_hip_error; }
+
+int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+                               const float *vals, const float *C, const float *D,
+                               const float *E, float *A, int64_t N, int64_t M, int64_t K,
+                               int64_t L, void *stream) {
+  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && K > 0 && !C) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && K > 0 && !D) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  const bool al = aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A);
+  WalkArgs a = base_args(rowptr, colidx, vals, N, K, L);
+  a.C = C;
+  a.D = D;
+  a.E = E;
+  a.out = A;
+  return run_walk(kFused, pick_fused(K, L, al), a, (hipStream_t)stream);
+}
+
+int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx, const float *vals,
+                    const float *C, const float *D, float *Y, int64_t N, int64_t M, int64_t K,
+                    void *stream) {
+  if (bad_size(N, M, K, 0)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals || !Y)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && K > 0 && !C) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && K > 0 && !D) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, 0);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0) return SPARSELNR_OK;
+  const bool al = aligned16(C) && aligned16(D);
+  WalkArgs a = base_args(rowptr, colidx, vals, N, K, 0);
+  a.C = C;
+  a.D = D;
+  a.out = Y;
+  return run_walk(kSddmm, pick_sddmm(K, al), a, (hipStream_t)stream);
+}
+
+int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx, const float *Y,
+                   const float *E, float *A, int64_t N, int64_t M, int64_t L, void *stream) {
+  if (bad_size(N, M, 0, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !Y)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, 0, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  const bool al = aligned16(E) && aligned16(A);
+  WalkArgs a = base_args(rowptr, colidx, Y, N, 0, L);
+  a.E = E;
+  a.out = A;
+  return run_walk(kSpmm, pick_spmm(L, al), a, (hipStream_t)stream);
+}
+
+int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+                                 const float *vals, const float *C, const float *D,
+                                 const float *E, float *Y, float *A, int64_t N, int64_t M,
+                                 int64_t K, int64_t L, void *stream) {
+  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals || !Y)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && K > 0 && !C) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && K > 0 && !D) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0) return SPARSELNR_OK;
+  rc = sparselnr_sddmm(rowptr, colidx, vals, C, D, Y, N, M, K, stream);
+  if (rc != SPARSELNR_OK) return rc;
+  return sparselnr_spmm(rowptr, colidx, Y, E, A, N, M, L, stream);
+}
+
+int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx, int64_t N, int64_t M,
+                           int64_t colidx_len, int64_t *nnz_out, void *stream) {
+  if (N < 0 || M < 0 || colidx_len < 0 || !rowptr) return SPARSELNR_ERR_INVALID_ARG;
+  if (colidx_len > 0 && !colidx) return SPARSELNR_ERR_INVALID_ARG;
+  if (N >= ((int64_t)1 << 31) - 1) return SPARSELNR_ERR_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  int32_t *flags = nullptr;
+  hipError_t e = hipMalloc(&flags, 2 * sizeof(int32_t));
+  if (e != hipSuccess) return hip_fail(e);
+  int32_t host[2] = {0, 0};
+  int rc = SPARSELNR_OK;
+  e = hipMemsetAsync(flags, 0, 2 * sizeof(int32_t), s);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(slnr::validate_csr_kernel, dim3(1024), dim3(256), 0, s, rowptr, colidx,
+                       N, M, colidx_len, flags);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipMemcpyAsync(&host[0], flags, sizeof(int32_t),
+                                          hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(&host[1], rowptr + N, sizeof(int32_t),
+                                          hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) rc = hip_fail(e);
+  hipError_t ef = hipFree(flags);
+  if (rc == SPARSELNR_OK && ef != hipSuccess) rc = hip_fail(ef);
+  if (rc != SPARSELNR_OK) return rc;
+  if (nnz_out) *nnz_out = host[1];
+  return host[0] == 0 ? SPARSELNR_OK : SPARSELNR_ERR_INVALID_CSR;
+}
+
+int sparselnr_release(void) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  int rc = SPARSELNR_OK;
+  int saved = 0;
+  (void)hipGetDevice(&saved);
+  for (auto &kv : g_workspace) {
+    if (!kv.second.ptr) continue;
+    hipError_t e = hipSetDevice(kv.first.first);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipFree(kv.second.ptr);
+    if (e != hipSuccess) rc = hip_fail(e);
+  }
+  g_workspace.clear();
+  (void)hipSetDevice(saved);
+  return rc;
+}
+
+}  // extern "C"

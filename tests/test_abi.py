@@ -1,0 +1,123 @@
+"""The C ABI: the library loads, exports every declared symbol, and rejects
+bad arguments before touching HIP (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2205_11622_amd as slnr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sparselnr.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sparselnr_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ["sparselnr_fused_sddmm_spmm", "sparselnr_unfused_sddmm_spmm",
+                     "sparselnr_sddmm", "sparselnr_spmm", "sparselnr_validate_csr",
+                     "sparselnr_status_string", "sparselnr_last_hip_error",
+                     "sparselnr_release", "sparselnr_abi_version"]:
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = slnr.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_names_match_the_abi():
+    for name in declared_functions():
+        assert hasattr(slnr, name), name
+
+
+def test_version_and_status_strings():
+    assert slnr.sparselnr_abi_version() == 1
+    for code in range(6):
+        s = slnr.sparselnr_status_string(code)
+        assert isinstance(s, str) and s
+    assert slnr.sparselnr_status_string(99) == "unknown status"
+    assert slnr.sparselnr_status_string(0) == "ok"
+
+
+NULL = None
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails validation first
+
+
+@pytest.mark.parametrize("args,code", [
+    # negative sizes
+    ((FAKE,) * 7 + (-1, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 7 + (4, -1, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 7 + (4, 4, -1, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 7 + (4, 4, 4, -1, NULL), slnr.ERR_INVALID_ARG),
+    # NULL arrays
+    ((NULL,) + (FAKE,) * 6 + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE, NULL) + (FAKE,) * 5 + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE, FAKE, NULL) + (FAKE,) * 4 + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 3 + (NULL,) + (FAKE,) * 3 + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 4 + (NULL,) + (FAKE,) * 2 + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 5 + (NULL, FAKE) + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    ((FAKE,) * 6 + (NULL,) + (4, 4, 4, 4, NULL), slnr.ERR_INVALID_ARG),
+    # too wide / too many rows
+    ((FAKE,) * 7 + (4, 4, 65537, 4, NULL), slnr.ERR_UNSUPPORTED),
+    ((FAKE,) * 7 + (4, 4, 4, 65537, NULL), slnr.ERR_UNSUPPORTED),
+    ((FAKE,) * 7 + (2**31, 4, 4, 4, NULL), slnr.ERR_UNSUPPORTED),
+    # empty problems need no HIP call at all
+    ((NULL,) * 7 + (0, 0, 0, 0, NULL), slnr.OK),
+    ((FAKE,) * 3 + (FAKE, FAKE, NULL, NULL) + (5, 5, 4, 0, NULL), slnr.OK),
+])
+def test_fused_argument_errors(args, code):
+    assert slnr.lib().sparselnr_fused_sddmm_spmm(*args) == code
+
+
+def test_other_entry_points_argument_errors():
+    L = slnr.lib()
+    assert L.sparselnr_sddmm(*(FAKE,) * 6, -1, 4, 4, NULL) == slnr.ERR_INVALID_ARG
+    assert L.sparselnr_sddmm(FAKE, FAKE, FAKE, FAKE, FAKE, NULL, 4, 4, 4, NULL) == slnr.ERR_INVALID_ARG
+    assert L.sparselnr_sddmm(*(NULL,) * 6, 0, 0, 0, NULL) == slnr.OK
+    assert L.sparselnr_spmm(*(FAKE,) * 5, 4, 4, -2, NULL) == slnr.ERR_INVALID_ARG
+    assert L.sparselnr_spmm(FAKE, FAKE, NULL, FAKE, FAKE, 4, 4, 4, NULL) == slnr.ERR_INVALID_ARG
+    assert L.sparselnr_spmm(*(FAKE,) * 5, 4, 4, 70000, NULL) == slnr.ERR_UNSUPPORTED
+    assert L.sparselnr_unfused_sddmm_spmm(*(FAKE,) * 6, NULL, FAKE, 4, 4, 4, 4, NULL) == \
+        slnr.ERR_INVALID_ARG
+    assert L.sparselnr_unfused_sddmm_spmm(*(FAKE,) * 8, 4, 4, 4, -4, NULL) == slnr.ERR_INVALID_ARG
+    nnz = ctypes.c_int64(0)
+    assert L.sparselnr_validate_csr(NULL, FAKE, 4, 4, 4, ctypes.byref(nnz), NULL) == \
+        slnr.ERR_INVALID_ARG
+    assert L.sparselnr_validate_csr(FAKE, FAKE, -1, 4, 4, ctypes.byref(nnz), NULL) == \
+        slnr.ERR_INVALID_ARG
+    assert L.sparselnr_validate_csr(FAKE, NULL, 4, 4, 4, ctypes.byref(nnz), NULL) == \
+        slnr.ERR_INVALID_ARG
+
+
+def test_no_hip_error_recorded_by_validation_failures():
+    slnr.lib().sparselnr_fused_sddmm_spmm(*(FAKE,) * 7, -1, 4, 4, 4, NULL)
+    assert slnr.sparselnr_last_hip_error() == 0
+
+
+def test_binding_refuses_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    rp = torch.zeros(3, dtype=torch.int32)
+    ci = torch.zeros(0, dtype=torch.int32)
+    v = torch.zeros(0)
+    C = torch.zeros(2, 4)
+    with pytest.raises(ValueError):
+        slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, C, C)
+
+
+def test_product_package_does_not_touch_the_oracle():
+    """The product path neither imports nor links the oracle or the input generators."""
+    pkg = os.path.join(ROOT, "paper_2205_11622_amd")
+    pat = re.compile(r"^\s*(import|from)\s+(oracle|synth)\b|liboracle|libsynth|oracle\.c", re.M)
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not pat.search(text), f

@@ -1,0 +1,234 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Tolerance (tests/parity.py): per row, max_l |A - Aref| <= 1e-4 * scale_i with
+scale_i = max_l sum_p |b_p| (sum_k |C_ik||D_jk|) |E_jl|; zero-scale rows must
+be exactly zero; NaN/Inf fail.  Structure (Y's order, which rows are written)
+must match exactly; invariants marked "bit" are compared bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2205_11622_amd as slnr
+import synth
+from tests.gpu_util import (check_A_rows, check_Y, fused, make_problem, power_law_lengths,
+                            sample_rows, unfused, upload)
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------- variants
+
+# (K, L): the first five have hand-tuned fast variants, the rest go through
+# the generic kernel (odd widths, K != L, tiny widths, wide L needing tiles).
+WIDTHS = [(32, 32), (64, 64), (128, 128), (256, 256), (16, 256),
+          (1, 1), (3, 5), (16, 16), (20, 36), (17, 300), (64, 520), (128, 64)]
+
+
+@pytest.mark.parametrize("K,L", WIDTHS)
+def test_fused_and_unfused_power_law(gpu, K, L):
+    # 3001 rows (ragged), ~30% empty, heavy rows spanning many workers
+    lengths = power_law_lengths(3001, seed=K * 1000 + L, cap=6000)
+    lengths[7] = 9000
+    p = make_problem(lengths, 2500, K, L, seed=K + L, dense="normal")
+    d = upload(p)
+    A = fused(d)
+    check_A_rows(p, A, what="fused A")
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au, what="unfused A")
+
+
+@pytest.mark.parametrize("K,L", [(32, 32), (128, 128), (16, 256), (5, 7)])
+def test_unsorted_and_duplicate_columns(gpu, K, L):
+    lengths = np.random.default_rng(3).integers(0, 60, size=777)
+    p = make_problem(lengths, 50, K, L, seed=5, dups=True, unsorted=True)
+    d = upload(p)
+    check_A_rows(p, fused(d))
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au)
+
+
+# ------------------------------------------------------------ edge cases
+
+def test_empty_matrix(gpu):
+    import torch
+    dev = gpu
+    rp = torch.zeros(1, dtype=torch.int32, device=dev)
+    ci = torch.zeros(0, dtype=torch.int32, device=dev)
+    v = torch.zeros(0, device=dev)
+    C = torch.zeros(0, 32, device=dev)
+    D = torch.zeros(5, 32, device=dev)
+    E = torch.zeros(5, 32, device=dev)
+    A = slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E)
+    assert A.shape == (0, 32)
+    Y, A = slnr.sparselnr_unfused_sddmm_spmm(rp, ci, v, C, D, E)
+    assert Y.shape == (0,) and A.shape == (0, 32)
+
+
+@pytest.mark.parametrize("K,L", [(32, 32), (128, 128), (16, 256), (3, 5)])
+def test_no_nonzeros_gives_zero_rows(gpu, K, L):
+    import torch
+    p = make_problem(np.zeros(1234, np.int64), 10, K, L)
+    d = upload(p)
+    A = torch.full((p.N, L), float("nan"), device=gpu)
+    slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"], A)
+    assert bool((A == 0).all())
+
+
+@pytest.mark.parametrize("K,L", [(128, 128), (16, 256), (64, 64), (9, 9)])
+def test_one_dense_row(gpu, K, L):
+    # a single row holding every column: the row is split over all workers
+    p = make_problem([100_000], 100_000, K, L, seed=2, dense="normal")
+    d = upload(p)
+    check_A_rows(p, fused(d))
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au)
+
+
+@pytest.mark.parametrize("K,L", [(32, 32), (128, 128)])
+def test_one_nonzero_rows_and_rectangular(gpu, K, L):
+    p = make_problem(np.ones(5000, np.int64), 77, K, L, seed=4)   # N != M
+    d = upload(p)
+    check_A_rows(p, fused(d))
+
+
+def test_K1_L1_and_K0(gpu):
+    lengths = power_law_lengths(500, seed=9, cap=300)
+    for K, L in [(1, 1), (1, 64), (64, 1)]:
+        p = make_problem(lengths, 400, K, L, seed=K + 2 * L)
+        check_A_rows(p, fused(upload(p)))
+    p = make_problem(lengths, 400, 0, 32)
+    A = fused(upload(p))
+    assert bool((A == 0).all())
+
+
+def test_misaligned_operands_take_the_generic_path(gpu):
+    import torch
+    lengths = power_law_lengths(700, seed=10, cap=500)
+    p = make_problem(lengths, 300, 32, 32, seed=11)
+    d = upload(p)
+    # views starting one float into a buffer: 4-byte aligned, not 16-byte aligned
+    def shifted(a):
+        buf = torch.empty(a.numel() + 1, dtype=a.dtype, device=a.device)
+        v = buf[1:].view(a.shape)
+        v.copy_(a)
+        return v
+    C, D, E = shifted(d["C"]), shifted(d["D"]), shifted(d["E"])
+    A = shifted(torch.zeros(p.N, 32, device=gpu))
+    slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], C, D, E, A)
+    check_A_rows(p, A)
+
+
+# ------------------------------------------------------------ invariants
+
+def test_deterministic_bit_exact(gpu):
+    p = make_problem(power_law_lengths(4000, seed=12, cap=8000), 3000, 128, 128, seed=12)
+    d = upload(p)
+    A1 = fused(d).clone()
+    A2 = fused(d)
+    assert bool(torch_equal(A1, A2))
+    Y1, Au1 = unfused(d)
+    Y1, Au1 = Y1.clone(), Au1.clone()
+    Y2, Au2 = unfused(d)
+    assert bool(torch_equal(Y1, Y2)) and bool(torch_equal(Au1, Au2))
+
+
+def torch_equal(a, b):
+    import torch
+    return torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def test_zero_B_and_power_of_two_scaling_bit_exact(gpu):
+    p = make_problem(power_law_lengths(3000, seed=13, cap=4000), 2000, 16, 256, seed=13)
+    d = upload(p)
+    A = fused(d).clone()
+    d2 = dict(d)
+    d2["vals"] = d["vals"] * 0
+    assert bool((fused(d2) == 0).all())
+    for key in ["vals", "C", "D", "E"]:
+        d2 = dict(d)
+        d2[key] = d[key] * 2
+        assert bool(torch_equal(fused(d2), A * 2)), key
+
+
+def test_column_order_within_rows(gpu):
+    p = make_problem(power_law_lengths(2000, seed=14, cap=3000), 1500, 64, 64, seed=14)
+    d = upload(p)
+    A = fused(d).cpu().numpy()
+    rng = np.random.default_rng(1)
+    perm = np.arange(p.nnz)
+    for i in range(p.N):
+        rng.shuffle(perm[p.rowptr[i]:p.rowptr[i + 1]])
+    q = synth.Problem("perm", p.N, p.M, p.K, p.L, p.rowptr, p.colidx[perm], p.vals[perm],
+                      p.C, p.D, p.E)
+    A2 = fused(upload(q)).cpu().numpy()
+    ref, scale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E)
+    from tests.parity import assert_rows_close
+    assert_rows_close(A2, A, 2 * scale)
+
+
+def test_validate_csr(gpu):
+    import torch
+    p = make_problem(power_law_lengths(300, seed=15, cap=100), 200, 8, 8)
+    d = upload(p)
+    assert slnr.sparselnr_validate_csr(d["rowptr"], d["colidx"], 200) == p.nnz
+    bad = d["colidx"].clone()
+    bad[p.nnz // 2] = 200
+    with pytest.raises(slnr.SparseLNRError) as e:
+        slnr.sparselnr_validate_csr(d["rowptr"], bad, 200)
+    assert e.value.status == slnr.ERR_INVALID_CSR
+    rp = d["rowptr"].clone()
+    rp[5], rp[6] = rp[6] + 1, rp[5]
+    with pytest.raises(slnr.SparseLNRError):
+        slnr.sparselnr_validate_csr(rp, d["colidx"], 200)
+    short = d["colidx"][: p.nnz // 2].clone()
+    with pytest.raises(slnr.SparseLNRError):
+        slnr.sparselnr_validate_csr(d["rowptr"], short, 200)
+
+
+def test_stream_argument_and_workspace_release(gpu):
+    import torch
+    p = make_problem(power_law_lengths(1000, seed=16, cap=2000), 900, 32, 32, seed=16)
+    d = upload(p)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        A = slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"],
+                                            d["E"], stream=s)
+    s.synchronize()
+    check_A_rows(p, A)
+    slnr.sparselnr_release()
+    check_A_rows(p, fused(d))
+
+
+# ------------------------------------------------- the five named workloads
+
+@pytest.mark.parametrize("name", ["tiny", "uniform"])
+def test_config_full(gpu, name):
+    p = synth.config(name)
+    d = upload(p)
+    check_A_rows(p, fused(d), what=name + " fused")
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au, what=name + " unfused")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", ["rmat1m", "rmat4m", "banded"])
+def test_config_sampled(gpu, name):
+    import torch
+    p = synth.config(name)
+    d = upload(p)
+    rows = sample_rows(p)
+    check_A_rows(p, fused(d), rows, what=name + " fused")
+    Y, Au = unfused(d)
+    check_Y(p, Y, rows[:500])
+    check_A_rows(p, Au, rows, what=name + " unfused")
+    # every row of A written: no NaN left from a NaN-filled output
+    A = torch.full((p.N, p.L), float("nan"), device=gpu)
+    slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"], A)
+    assert not bool(torch.isnan(A).any())
+    del A, Y, Au, d
+    torch.cuda.empty_cache()

@@ -1,0 +1,134 @@
+"""Host model of the library's merge-path work split and carry fixup.
+
+The GPU kernels split the merged sequence (N row ends + nnz nonzeros) into
+equal slices, one per worker; rows straddling slices leave head / tail
+partials that a fixup kernel adds in slice order.  This test re-enacts those
+rules in Python on many CSR shapes (empty rows, one huge row, rows ending
+exactly on a slice boundary, more workers than items) and checks that every
+nonzero is consumed exactly once, every row of A is written exactly once,
+and every index stays inside its buffer, before any kernel runs on a GPU.
+"""
+import numpy as np
+import pytest
+
+
+def mp_search(rowptr, N, nnz, d):
+    lo, hi = max(0, d - nnz), min(d, N)
+    while lo < hi:
+        mid = (lo + hi + 1) >> 1
+        if rowptr[mid] + mid <= d:
+            lo = mid
+        else:
+            hi = mid - 1
+    return lo
+
+
+def simulate(rowptr, workers, min_chunk, L=3, rng=None):
+    """Returns (A, writes) computed through the slice / carry / fixup rules."""
+    N = rowptr.size - 1
+    nnz = int(rowptr[N])
+    items = N + nnz
+    S = max(-(-items // workers), min_chunk)
+    rng = rng or np.random.default_rng(0)
+    contrib = rng.integers(-5, 6, size=(nnz, L)).astype(np.float64)  # y_p * E_j, exact ints
+    A = np.full((N, L), np.nan)
+    writes = np.zeros(N, dtype=int)
+    consumed = np.zeros(nnz, dtype=int)
+    carry = np.full((workers, 2, L), np.nan)
+    meta = np.full((workers, 2), -7, dtype=np.int64)
+    for w in range(workers):
+        d0 = w * S
+        if d0 >= items:
+            meta[w] = (-1, -1)
+            continue
+        d1 = min(d0 + S, items)
+        i0 = mp_search(rowptr, N, nnz, d0)
+        p0 = d0 - i0
+        i1 = mp_search(rowptr, N, nnz, d1)
+        p1 = d1 - i1
+        assert 0 <= i0 <= i1 <= N and 0 <= p0 <= p1 <= nnz
+        assert rowptr[i0] <= p0 <= (rowptr[i0 + 1] if i0 < N else nnz)
+        head = i0 < i1 and p0 > rowptr[i0]
+        i, p = i0, p0
+        while True:
+            has_end = i < i1
+            if not has_end and i >= N:
+                break
+            r_end = rowptr[i + 1] if has_end else p1
+            acc = np.zeros(L)
+            while p < r_end:
+                assert 0 <= p < p1 <= nnz
+                consumed[p] += 1
+                acc += contrib[p]
+                p += 1
+            if not has_end:
+                carry[w, 1] = acc
+            elif i == i0 and head:
+                carry[w, 0] = acc
+            else:
+                assert 0 <= i < N
+                A[i] = acc
+                writes[i] += 1
+            if not has_end:
+                break
+            i += 1
+        meta[w] = (i1 if i1 < N else -1, i0 if head else -1)
+    # fixup
+    for c in range(workers):
+        r = meta[c, 1]
+        if r < 0:
+            continue
+        first = c
+        while first - 1 >= 0 and meta[first - 1, 0] == r:
+            first -= 1
+        s = np.zeros(L)
+        for cc in range(first, c):
+            assert not np.isnan(carry[cc, 1]).any(), "tail slot read before written"
+            s += carry[cc, 1]
+        assert not np.isnan(carry[c, 0]).any()
+        s += carry[c, 0]
+        A[r] = s
+        writes[r] += 1
+    ref = np.zeros((N, L))
+    for i in range(N):
+        ref[i] = contrib[rowptr[i]:rowptr[i + 1]].sum(axis=0)
+    return A, writes, consumed, ref
+
+
+def csr_from_lengths(lengths):
+    rowptr = np.zeros(len(lengths) + 1, dtype=np.int64)
+    rowptr[1:] = np.cumsum(lengths)
+    return rowptr
+
+
+CASES = {
+    "uniform": [10] * 50,
+    "empty": [0] * 17,
+    "one_huge": [0, 3, 1000, 0, 2],
+    "power_law": [int(x) for x in (np.random.default_rng(1).pareto(1.2, 300) * 3)],
+    "mixed_empty": [0, 0, 5, 0, 0, 0, 64, 1, 0, 33, 0],
+    "single_row": [257],
+    "single_empty": [0],
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+@pytest.mark.parametrize("workers,min_chunk", [(1, 1), (3, 1), (7, 2), (64, 1), (64, 32),
+                                                (1000, 1), (5, 1000)])
+def test_every_row_once(name, workers, min_chunk):
+    rowptr = csr_from_lengths(CASES[name])
+    A, writes, consumed, ref = simulate(rowptr, workers, min_chunk)
+    assert np.all(consumed == 1)
+    assert np.all(writes == 1)
+    assert np.array_equal(A, ref)
+
+
+def test_rows_ending_on_slice_boundaries():
+    # every slice boundary lands exactly on a row end, on a row start, or mid-row
+    for S in range(1, 12):
+        lengths = [S - 1, S, 2 * S, 0, 0, S + 1, 1]
+        rowptr = csr_from_lengths(lengths)
+        items = len(lengths) + rowptr[-1]
+        workers = -(-items // S)
+        A, writes, consumed, ref = simulate(rowptr, workers, 1)
+        assert np.all(consumed == 1) and np.all(writes == 1) and np.array_equal(A, ref)
