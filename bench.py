@@ -60,6 +60,9 @@ def main() -> int:
     ap.add_argument("--config", default="rmat1m")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after timing, run three plain 1 GiB device copies (torch copy_), the "
+                         "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -126,6 +129,14 @@ def main() -> int:
         print("# unfused: %.4f ms/call; fused rerun %.4f ms" % (unf["ms_per_call"],
                                                                unf["fused_ms_rerun"]),
               file=sys.stderr, flush=True)
+
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     nnz = p.nnz
     model_bytes = p.model_bytes()

@@ -181,7 +181,9 @@ def test_validate_csr(gpu):
         slnr.sparselnr_validate_csr(d["rowptr"], bad, 200)
     assert e.value.status == slnr.ERR_INVALID_CSR
     rp = d["rowptr"].clone()
-    rp[5], rp[6] = rp[6] + 1, rp[5]
+    a, b = int(rp[5]), int(rp[6])
+    rp[5] = b + 1          # rowptr[5] > rowptr[6]: decreasing
+    rp[6] = a
     with pytest.raises(slnr.SparseLNRError):
         slnr.sparselnr_validate_csr(rp, d["colidx"], 200)
     short = d["colidx"][: p.nnz // 2].clone()
