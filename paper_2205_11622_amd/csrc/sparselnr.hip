@@ -19,8 +19,18 @@ using slnr::WalkArgs;
 thread_local int g_last_hip_error = 0;
 
 constexpr int kBlock = 256;       // threads per block (4 waves)
-constexpr int kMinChunk = 32;     // smallest merge-path slice per worker
+#ifndef SLNR_MIN_CHUNK
+#define SLNR_MIN_CHUNK 64
+#endif
+constexpr int kMinChunk = SLNR_MIN_CHUNK;  // smallest merge-path slice per worker
 constexpr int kXcds = 8;          // MI355X deals blocks over 8 XCDs
+#ifndef SLNR_GRID_FACTOR
+#define SLNR_GRID_FACTOR 8
+#endif
+#ifndef SLNR_XCD_REMAP
+#define SLNR_XCD_REMAP 1
+#endif
+constexpr int kGridFactor = SLNR_GRID_FACTOR;
 constexpr int kGenericLT = 4;     // generic path: 4 x 64 = 256 columns per tile
 
 int hip_fail(hipError_t e) {
@@ -36,7 +46,7 @@ struct Workspace {
 std::mutex g_mu;
 std::map<int, int> g_cus;                                    // device -> CUs
 std::map<std::pair<int, uintptr_t>, int> g_occupancy;        // (device, kernel) -> blocks/CU
-int g_grid_factor = 0;                                       // resident grids per launch
+int g_grid_factor = 0;  // resident grids per launch (SPARSELNR_GRID_FACTOR; -1: by size)
 std::map<std::pair<int, uintptr_t>, Workspace> g_workspace;  // (device, stream)
 
 int current_device(int *dev) {
@@ -91,6 +101,9 @@ int get_workspace(int dev, hipStream_t stream, size_t bytes, void **out) {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+// The fast kernels address gathered rows with 32-bit byte offsets.
+bool offsets32(int64_t rows, int64_t width) { return rows * width * 4 < ((int64_t)1 << 32); }
+
 // ----------------------------------------------------------- variants
 
 enum Mode { kFused = slnr::kFused, kSddmm = slnr::kSddmm, kSpmm = slnr::kSpmm };
@@ -103,10 +116,10 @@ struct Variant {
   bool generic = true; // generic kernel (l-tiles of 256 columns)
 };
 
-template <int MODE, int W, int NB, int KV, int LV, int U>
+template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1>
 Variant fast() {
   Variant v;
-  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, U>;
+  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, SCHED, U>;
   v.W = W;
   v.generic = false;
   return v;
@@ -121,37 +134,58 @@ Variant generic() {
   return v;
 }
 
+// Gather schedule of the fused kernels and of the unfused (SDDMM, SpMM)
+// kernels, each set to what measured fastest for it on MI355X: the fused
+// kernels pace their gathers, the unfused ones pipeline them.  Nonzeros per
+// step of the paced schedule: 8 for the 128-wide rows, 4 otherwise.
+#ifndef SLNR_FUSED_SCHED
+#define SLNR_FUSED_SCHED 1
+#endif
+#ifndef SLNR_UNFUSED_SCHED
+#define SLNR_UNFUSED_SCHED 0
+#endif
+#ifndef SLNR_PACED_U
+#define SLNR_PACED_U 4
+#endif
+#ifndef SLNR_PACED_U128
+#define SLNR_PACED_U128 8
+#endif
+constexpr int kFS = SLNR_FUSED_SCHED;
+constexpr int kUS = SLNR_UNFUSED_SCHED;
+constexpr int kPU = SLNR_PACED_U;
+constexpr int kPU128 = SLNR_PACED_U128;
+
 // Fast variants exist for the widths of the benchmark workloads: K = L in
 // {32, 64, 128, 256} (one 16-byte slice of C/D and of E/A per lane) and the
 // asymmetric K = 16, L = 256 (4-lane dot products, 16 per producer pass).
 Variant pick_fused(int64_t K, int64_t L, bool al) {
   if (al) {
-    if (K == 32 && L == 32) return fast<kFused, 8, 1, 4, 4, 4>();
-    if (K == 64 && L == 64) return fast<kFused, 16, 1, 4, 4, 4>();
-    if (K == 128 && L == 128) return fast<kFused, 32, 1, 4, 4, 4>();
-    if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, 4>();
-    if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, 16>();
+    if (K == 32 && L == 32) return fast<kFused, 8, 1, 4, 4, kFS, kPU>();
+    if (K == 64 && L == 64) return fast<kFused, 16, 1, 4, 4, kFS, kPU>();
+    if (K == 128 && L == 128) return fast<kFused, 32, 1, 4, 4, kFS, kPU128>();
+    if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, kFS, kPU>();
+    if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, kFS, 16>();
   }
   return generic<kFused>();
 }
 
 Variant pick_sddmm(int64_t K, bool al) {
   if (al) {
-    if (K == 16) return fast<kSddmm, 64, 16, 4, 4, 16>();
-    if (K == 32) return fast<kSddmm, 8, 1, 4, 4, 4>();
-    if (K == 64) return fast<kSddmm, 16, 1, 4, 4, 4>();
-    if (K == 128) return fast<kSddmm, 32, 1, 4, 4, 4>();
-    if (K == 256) return fast<kSddmm, 64, 1, 4, 4, 4>();
+    if (K == 16) return fast<kSddmm, 64, 16, 4, 4, kUS, 16>();
+    if (K == 32) return fast<kSddmm, 8, 1, 4, 4, kUS, kPU>();
+    if (K == 64) return fast<kSddmm, 16, 1, 4, 4, kUS, kPU>();
+    if (K == 128) return fast<kSddmm, 32, 1, 4, 4, kUS, kPU128>();
+    if (K == 256) return fast<kSddmm, 64, 1, 4, 4, kUS, kPU>();
   }
   return generic<kSddmm>();
 }
 
 Variant pick_spmm(int64_t L, bool al) {
   if (al) {
-    if (L == 32) return fast<kSpmm, 8, 1, 4, 4, 4>();
-    if (L == 64) return fast<kSpmm, 16, 1, 4, 4, 4>();
-    if (L == 128) return fast<kSpmm, 32, 1, 4, 4, 4>();
-    if (L == 256) return fast<kSpmm, 64, 1, 4, 4, 4>();
+    if (L == 32) return fast<kSpmm, 8, 1, 4, 4, kUS, kPU>();
+    if (L == 64) return fast<kSpmm, 16, 1, 4, 4, kUS, kPU>();
+    if (L == 128) return fast<kSpmm, 32, 1, 4, 4, kUS, kPU128>();
+    if (L == 256) return fast<kSpmm, 64, 1, 4, 4, kUS, kPU>();
   }
   return generic<kSpmm>();
 }
@@ -167,8 +201,8 @@ int blocks_per_cu(int dev, KernelFn fn, int *out) {
   std::lock_guard<std::mutex> lock(g_mu);
   if (g_grid_factor == 0) {
     const char *env = getenv("SPARSELNR_GRID_FACTOR");
-    const int f = env ? atoi(env) : 1;
-    g_grid_factor = f >= 1 && f <= 64 ? f : 1;
+    const int f = env ? atoi(env) : -1;
+    g_grid_factor = f >= 1 && f <= 64 ? f : -1;  // -1: chosen per call
   }
   auto key = std::make_pair(dev, (uintptr_t)fn);
   auto it = g_occupancy.find(key);
@@ -185,15 +219,23 @@ int blocks_per_cu(int dev, KernelFn fn, int *out) {
   return SPARSELNR_OK;
 }
 
-// One resident grid (times SPARSELNR_GRID_FACTOR): every worker starts at
-// once and owns an equal merge-path slice.
-Grid make_grid(int cus, int per_cu, int W) {
+// The grid is `factor` resident grids.  Large matrices use kGridFactor:
+// many more slices than resident workers, so the blocks resident on an XCD
+// at any moment walk a compact window of rows (neighbouring rows of banded
+// matrices share their D/E rows in L2) and the dispatcher balances the tail.
+// Small matrices (fewer than 8 rows per resident worker) use one resident
+// grid, because extra blocks would only find empty slices.
+Grid make_grid(int cus, int per_cu, int W, int64_t N) {
   Grid g;
-  int blocks = cus * per_cu * g_grid_factor;
+  const int64_t resident_blocks = (int64_t)cus * per_cu;
+  const int64_t resident_workers = resident_blocks * (kBlock / 64) * (64 / W);
+  int factor = g_grid_factor;
+  if (factor < 1) factor = N >= 8 * resident_workers ? kGridFactor : 1;
+  int blocks = (int)(resident_blocks * factor);
   blocks = ((blocks + kXcds - 1) / kXcds) * kXcds;
   g.blocks = blocks;
   g.workers = blocks * (kBlock / 64) * (64 / W);
-  g.xcd_span = blocks / kXcds;
+  g.xcd_span = SLNR_XCD_REMAP ? blocks / kXcds : 0;
   return g;
 }
 
@@ -204,7 +246,7 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
   if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
   int per_cu = 1;
   if ((rc = blocks_per_cu(dev, v.fn, &per_cu)) != SPARSELNR_OK) return rc;
-  const Grid g = make_grid(cus, per_cu, v.W);
+  const Grid g = make_grid(cus, per_cu, v.W, a.N);
   a.workers = g.workers;
   a.min_chunk = kMinChunk;
   a.xcd_span = g.xcd_span;
@@ -231,9 +273,7 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
     if (e != hipSuccess) return hip_fail(e);
     if (mode != kSddmm) {
       const int fix_blocks = (g.workers + (kBlock / 64) - 1) / (kBlock / 64);
-      hipLaunchKernelGGL(slnr::carry_fixup, dim3(fix_blocks), dim3(kBlock), 0, stream,
-                         (const float *)a.carry, (const int32_t *)a.meta, a.out, a.workers,
-                         a.Lw, a.L, a.l0);
+      hipLaunchKernelGGL(slnr::carry_fixup, dim3(fix_blocks), dim3(kBlock), 0, stream, a);
       e = hipGetLastError();
       if (e != hipSuccess) return hip_fail(e);
     }
@@ -298,7 +338,8 @@ int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
   int rc = check_range(N, M, K, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
-  const bool al = aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A);
+  const bool al = aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A) &&
+                  offsets32(M, K) && offsets32(M, L);
   WalkArgs a = base_args(rowptr, colidx, vals, N, K, L);
   a.C = C;
   a.D = D;
@@ -317,7 +358,7 @@ int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx, const float *v
   int rc = check_range(N, M, K, 0);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0) return SPARSELNR_OK;
-  const bool al = aligned16(C) && aligned16(D);
+  const bool al = aligned16(C) && aligned16(D) && offsets32(M, K);
   WalkArgs a = base_args(rowptr, colidx, vals, N, K, 0);
   a.C = C;
   a.D = D;
@@ -334,7 +375,7 @@ int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx, const float *Y,
   int rc = check_range(N, M, 0, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
-  const bool al = aligned16(E) && aligned16(A);
+  const bool al = aligned16(E) && aligned16(A) && offsets32(M, L);
   WalkArgs a = base_args(rowptr, colidx, Y, N, 0, L);
   a.E = E;
   a.out = A;

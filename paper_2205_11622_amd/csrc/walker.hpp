@@ -27,9 +27,33 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#ifndef SLNR_NT
+#define SLNR_NT 1
+#endif
+
 namespace slnr {
 
+// Streams read or written once per call carry the nontemporal hint.
+constexpr bool kNT = SLNR_NT != 0;
+
 enum Mode : int { kFused = 0, kSddmm = 1, kSpmm = 2 };
+
+// Gather schedules of a step of nonzeros:
+//  kPipelined  a depth-2 software pipeline (nonzero u's rows in flight while
+//              u-1 is reduced and applied); few registers, high occupancy.
+//  kPaced      all index broadcasts of the step first, then the gathers one
+//              nonzero at a time, each issued once the previous nonzero's D
+//              row has arrived, then all arithmetic.  Fewer requests in
+//              flight per worker keeps workers of an XCD in step, which keeps
+//              rows shared by neighbouring rows (banded matrices) in L2.
+enum Sched : int { kPipelined = 0, kPaced = 1 };
+
+// s_waitcnt immediate (gfx9 encoding) waiting for vmcnt <= V only.
+template <int V>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(V >= 0 && V < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 struct WalkArgs {
   const int32_t *rowptr;
@@ -87,95 +111,173 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
-template <int V>
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef float f2_t __attribute__((ext_vector_type(2)));
+
+// Loads V consecutive floats.  NT marks a stream read once per call
+// (nontemporal hint: the line is not kept in L2 ahead of the D/E rows that
+// are gathered again and again).
+template <int V, bool NT = false>
 __device__ __forceinline__ void ldv(float (&r)[V], const float *p) {
   if constexpr (V % 4 == 0) {
 #pragma unroll
     for (int t = 0; t < V / 4; ++t) {
-      const float4 x = reinterpret_cast<const float4 *>(p)[t];
-      r[4 * t] = x.x; r[4 * t + 1] = x.y; r[4 * t + 2] = x.z; r[4 * t + 3] = x.w;
+      const f4_t *q = reinterpret_cast<const f4_t *>(p) + t;
+      const f4_t x = NT ? __builtin_nontemporal_load(q) : *q;
+      r[4 * t] = x[0]; r[4 * t + 1] = x[1]; r[4 * t + 2] = x[2]; r[4 * t + 3] = x[3];
     }
   } else if constexpr (V % 2 == 0) {
 #pragma unroll
     for (int t = 0; t < V / 2; ++t) {
-      const float2 x = reinterpret_cast<const float2 *>(p)[t];
-      r[2 * t] = x.x; r[2 * t + 1] = x.y;
+      const f2_t *q = reinterpret_cast<const f2_t *>(p) + t;
+      const f2_t x = NT ? __builtin_nontemporal_load(q) : *q;
+      r[2 * t] = x[0]; r[2 * t + 1] = x[1];
     }
   } else {
 #pragma unroll
-    for (int t = 0; t < V; ++t) r[t] = p[t];
+    for (int t = 0; t < V; ++t) r[t] = NT ? __builtin_nontemporal_load(p + t) : p[t];
   }
 }
 
-template <int V>
+template <int V, bool NT = false>
 __device__ __forceinline__ void stv(float *p, const float (&r)[V]) {
   if constexpr (V % 4 == 0) {
 #pragma unroll
-    for (int t = 0; t < V / 4; ++t)
-      reinterpret_cast<float4 *>(p)[t] = make_float4(r[4 * t], r[4 * t + 1], r[4 * t + 2], r[4 * t + 3]);
+    for (int t = 0; t < V / 4; ++t) {
+      f4_t x;
+      x[0] = r[4 * t]; x[1] = r[4 * t + 1]; x[2] = r[4 * t + 2]; x[3] = r[4 * t + 3];
+      f4_t *q = reinterpret_cast<f4_t *>(p) + t;
+      if constexpr (NT) __builtin_nontemporal_store(x, q);
+      else *q = x;
+    }
   } else if constexpr (V % 2 == 0) {
 #pragma unroll
-    for (int t = 0; t < V / 2; ++t)
-      reinterpret_cast<float2 *>(p)[t] = make_float2(r[2 * t], r[2 * t + 1]);
+    for (int t = 0; t < V / 2; ++t) {
+      f2_t x;
+      x[0] = r[2 * t]; x[1] = r[2 * t + 1];
+      f2_t *q = reinterpret_cast<f2_t *>(p) + t;
+      if constexpr (NT) __builtin_nontemporal_store(x, q);
+      else *q = x;
+    }
   } else {
 #pragma unroll
-    for (int t = 0; t < V; ++t) p[t] = r[t];
+    for (int t = 0; t < V; ++t) {
+      if constexpr (NT) __builtin_nontemporal_store(r[t], p + t);
+      else p[t] = r[t];
+    }
   }
+}
+
+// Loads V floats at byte offset `off` from `base`.  The offset is 32-bit
+// (the host only selects the fast kernels when every gathered array is
+// below 4 GiB), so the address is formed from the kernel-argument base in
+// SGPRs plus one VGPR.
+template <int V>
+__device__ __forceinline__ void ldv_off(float (&r)[V], const float *__restrict__ base,
+                                        uint32_t off) {
+  ldv<V>(r, reinterpret_cast<const float *>(reinterpret_cast<const char *>(base) + off));
+}
+
+template <typename T>
+__device__ __forceinline__ T ld_stream(const T *p) {
+  return __builtin_nontemporal_load(p);
 }
 
 // ------------------------------------------------------------ merge path
 
 // Largest row i in [max(0, d - nnz), min(d, N)] with rowptr[i] + i <= d: the
 // merge-path coordinate (i row ends, d - i nonzeros consumed) of diagonal d.
-// rowptr[i] + i is strictly increasing, so this is a plain bisection.
-__device__ __forceinline__ int64_t mp_search(const int32_t *rowptr, int64_t N,
-                                             int64_t nnz, int64_t d) {
-  int64_t lo = d > nnz ? d - nnz : 0;
+// rowptr[i] + i is strictly increasing in i.  The G lanes of a worker probe
+// G points of the current interval at once and keep the sub-interval the
+// ballot points to, so the search takes log_G(N) steps instead of log_2(N)
+// dependent loads.  All lanes of the group return the same value.
+template <int G>
+__device__ __forceinline__ int64_t mp_search(const int32_t *rowptr, int64_t N, int64_t nnz,
+                                             int64_t d) {
+  const int lane = threadIdx.x & 63;
+  const int glane = lane & (G - 1);
+  const int gbase = lane - glane;
+  int64_t lo = d > nnz ? d - nnz : 0;  // rowptr[lo] + lo <= d always holds
   int64_t hi = d < N ? d : N;
   while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if ((int64_t)rowptr[mid] + mid <= d) lo = mid;
-    else hi = mid - 1;
+    const int64_t step = (hi - lo + G - 1) / G;
+    int64_t x = lo + (int64_t)(glane + 1) * step;
+    if (x > hi) x = hi;
+    const bool ok = (int64_t)rowptr[x] + x <= d;
+    const uint64_t ball = __ballot(ok);
+    const uint64_t bits = G == 64 ? ball : (ball >> gbase) & ((1ull << G) - 1);
+    const int m = (~bits == 0) ? 64 : __builtin_ctzll(~bits);  // probes 0..m-1 hold
+    const int64_t xm1 = lo + (int64_t)m * step;                 // probe m-1 (if m > 0)
+    const int64_t xm = lo + (int64_t)(m + 1) * step;            // probe m (if m < G)
+    if (m > 0) lo = xm1 < hi ? xm1 : hi;
+    if (m < G) hi = (xm < hi ? xm : hi) - 1;
   }
   return lo;
 }
 
 struct Slice {
+  int64_t id;              // slice index in merge order
   int64_t i0, p0, i1, p1;  // start and end coordinates
   bool head;               // row i0 began in an earlier slice and ends here
   bool active;
 };
 
-__device__ __forceinline__ int64_t logical_block(const WalkArgs &a) {
-  // Blocks are dealt round-robin over the XCDs; remap so that each XCD works
-  // through one contiguous range of slices (neighbouring rows share L2).
-  if (a.xcd_span > 0)
-    return (int64_t)(blockIdx.x % a.xcds) * a.xcd_span + blockIdx.x / a.xcds;
-  return blockIdx.x;
-}
-
-__device__ __forceinline__ Slice make_slice(const WalkArgs &a, int64_t worker) {
-  Slice s;
-  const int64_t N = a.N;
-  const int64_t nnz = a.rowptr[N];
-  const int64_t items = N + nnz;
+// Slices are S = max(min_chunk, ceil(items / workers)) items long, so small
+// inputs use only the first ns = ceil(items / S) of them.  With the XCD
+// remap, XCD x (blocks are dealt round-robin over the XCDs) takes the
+// contiguous run of slices [x * ns / xcds, (x + 1) * ns / xcds), so that the
+// workers sharing an L2 walk neighbouring rows and every XCD gets an equal
+// share however small the input.
+__device__ __forceinline__ void slice_count(const WalkArgs &a, int64_t *S_out, int64_t *ns_out,
+                                            int64_t *items_out, int64_t *nnz_out) {
+  const int64_t nnz = a.rowptr[a.N];
+  const int64_t items = a.N + nnz;
   int64_t S = (items + a.workers - 1) / a.workers;
   if (S < a.min_chunk) S = a.min_chunk;
-  const int64_t d0 = worker * S;
-  s.active = d0 < items;
-  if (!s.active) {
-    s.i0 = s.p0 = s.i1 = s.p1 = 0;
-    s.head = false;
-    return s;
+  *S_out = S;
+  *ns_out = (items + S - 1) / S;
+  *items_out = items;
+  *nnz_out = nnz;
+}
+
+template <int W>
+__device__ __forceinline__ Slice make_slice(const WalkArgs &a) {
+  Slice s;
+  int64_t S, ns, items, nnz;
+  slice_count(a, &S, &ns, &items, &nnz);
+  constexpr int kWorkersPerWave = 64 / W;
+  const int64_t wpb = (int64_t)(blockDim.x >> 6) * kWorkersPerWave;
+  const int64_t local = (threadIdx.x >> 6) * kWorkersPerWave + (threadIdx.x & 63) / W;
+  if (a.xcd_span > 0) {
+    const int64_t xcd = blockIdx.x % a.xcds;
+    const int64_t in_xcd = (int64_t)(blockIdx.x / a.xcds) * wpb + local;
+    const int64_t per_xcd = (ns + a.xcds - 1) / a.xcds;
+    s.id = xcd * per_xcd + in_xcd;
+    s.active = in_xcd < per_xcd && s.id < ns;
+  } else {
+    s.id = (int64_t)blockIdx.x * wpb + local;
+    s.active = s.id < ns;
   }
+  s.i0 = s.p0 = s.i1 = s.p1 = 0;
+  s.head = false;
+  if (!s.active) return s;
+  const int64_t d0 = s.id * S;
   const int64_t d1 = d0 + S < items ? d0 + S : items;
-  s.i0 = mp_search(a.rowptr, N, nnz, d0);
+  s.i0 = mp_search<W>(a.rowptr, a.N, nnz, d0);
   s.p0 = d0 - s.i0;
-  s.i1 = mp_search(a.rowptr, N, nnz, d1);
+  s.i1 = mp_search<W>(a.rowptr, a.N, nnz, d1);
   s.p1 = d1 - s.i1;
   s.head = (s.i0 < s.i1) && (s.p0 > (int64_t)a.rowptr[s.i0]);
   return s;
 }
+
+// Registers holding one nonzero's gathered rows.
+template <int MODE, int KV, int LV>
+struct Gather {
+  float d[MODE == kSpmm ? 1 : KV];
+  float e[MODE == kSddmm ? 1 : LV];
+  float b;
+};
 
 // ------------------------------------------------------ fast-path kernel
 //
@@ -183,28 +285,29 @@ __device__ __forceinline__ Slice make_slice(const WalkArgs &a, int64_t worker) {
 // NB  nonzeros per producer pass; PS = W / NB lanes form one dot product.
 // KV  floats of C_i / D_j per producer lane (K = PS * KV).
 // LV  floats of E_j / A_i per lane (L = W * LV).
-// U   nonzeros per loop step (their gathers are all in flight together).
-template <int MODE, int W, int NB, int KV, int LV, int U>
+// SCHED, U  gather schedule and, for kPaced, the nonzeros per step.
+//
+// Per worker the state is group-uniform (all W lanes agree on i, p, n), so
+// lane-group divergence inside a wave only masks whole groups.  Three small
+// windows, one entry per lane, keep the dependent loads off the critical
+// path: rowptr (row ends), colidx and vals.  C_i, the CSR arrays and A are
+// streamed once per call and carry the nontemporal hint; the gathered D_j and
+// E_j rows are plain loads so the hot columns stay in L2.
+template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U>
 __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
   constexpr int PS = W / NB;
   static_assert(W >= 4 && W <= 64 && (W & (W - 1)) == 0, "W");
   static_assert(NB >= 1 && W % NB == 0, "NB");
-  static_assert(NB == 1 || U == NB, "a producer pass handles one step");
-  static_assert(U <= W, "the index window must cover a step");
+  static_assert(SCHED == kPipelined || (U >= 1 && U <= W && (NB == 1 || U == NB)), "U");
   const int lane = threadIdx.x & 63;
   const int glane = lane & (W - 1);
   const int gbase = lane - glane;
   const int q = glane % PS;   // k-slice of this lane in its dot product
   const int sub = glane / PS; // which nonzero of a producer pass (NB > 1)
-  const int64_t worker =
-      (logical_block(a) * (blockDim.x >> 6) + (threadIdx.x >> 6)) * (64 / W) + lane / W;
-  if (worker >= a.workers) return;
+  const Slice s = make_slice<W>(a);
+  if (!s.active) return;
+  const int64_t worker = s.id;  // carry slots and metadata are per slice
   int32_t *meta = a.meta + 2 * worker;
-  const Slice s = make_slice(a, worker);
-  if (!s.active) {
-    if (MODE != kSddmm && glane == 0) { meta[0] = -1; meta[1] = -1; }
-    return;
-  }
   const int32_t *__restrict__ rowptr = a.rowptr;
   const int32_t *__restrict__ colidx = a.colidx;
   const float *__restrict__ vals = a.vals;
@@ -213,41 +316,67 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
   const float *__restrict__ Em = a.E;
   float *__restrict__ out = a.out;
   const int64_t K = a.K, L = a.L, N = a.N;
+  constexpr int64_t kFar = -((int64_t)1 << 40);
+  // byte strides of D and E rows and this lane's byte offset inside a row
+  const uint32_t strideD = (uint32_t)K * 4u, strideE = (uint32_t)L * 4u;
+  const uint32_t offD = (uint32_t)(q * KV) * 4u, offE = (uint32_t)(glane * LV) * 4u;
 
   int64_t i = s.i0, p = s.p0;
-  int64_t wb = -(int64_t)(1 << 30);  // base of the index window
-  int wj = 0;                        // colidx[wb + glane]
-  float wv = 0.f;                    // vals[wb + glane]
+  int64_t rb = kFar;  // rowptr window: wr = rowptr[rb + glane]
+  int wr = 0;
+  int64_t wb = kFar;  // nonzero window: wj = colidx[wb + glane], wv = vals[wb + glane]
+  int wj = 0;
+  float wv = 0.f;
   while (true) {
     const bool has_end = i < s.i1;
     if (!has_end && i >= N) break;
-    const int64_t r_end = has_end ? (int64_t)rowptr[i + 1] : s.p1;
+    int64_t r_end = s.p1;
+    if (has_end) {
+      if (i + 1 >= rb + W) {
+        rb = i + 1;
+        if (rb + glane <= N) wr = kNT ? ld_stream(rowptr + rb + glane) : rowptr[rb + glane];
+      }
+      r_end = bperm_i(gbase + (int)(i + 1 - rb), wr);
+    }
     float acc[LV];
 #pragma unroll
     for (int v = 0; v < LV; ++v) acc[v] = 0.f;
     float c[KV];
 #pragma unroll
     for (int v = 0; v < KV; ++v) c[v] = 0.f;
-    if (MODE != kSpmm && p < r_end) ldv<KV>(c, Cm + i * K + q * KV);
+    if (MODE != kSpmm && p < r_end) ldv<KV, kNT>(c, Cm + i * K + q * KV);
     while (p < r_end) {
-      const int n = (int)(r_end - p < U ? r_end - p : U);
-      if (p + n > wb + W) {  // refill the index window
+      if (p >= wb + W) {  // refill the nonzero window
         wb = p;
         const int64_t pw = wb + glane;
-        if (pw < s.p1) { wj = colidx[pw]; wv = vals[pw]; }
+        if (pw < s.p1) {
+          wj = kNT ? ld_stream(colidx + pw) : colidx[pw];
+          wv = kNT ? ld_stream(vals + pw) : vals[pw];
+        }
       }
+      // this step: the row's nonzeros inside the window (at most NB for a
+      // producer pass of the multi-dot variant)
+      int n = (int)(r_end - p < wb + W - p ? r_end - p : wb + W - p);
+      if (NB > 1 && n > NB) n = NB;
+      if (SCHED == kPaced && n > U) n = U;
       const int off = (int)(p - wb);
-      if constexpr (NB == 1) {
+      if constexpr (NB == 1 && SCHED == kPaced) {
+        uint32_t jj[U];
+        float bb[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {  // lanes past n read stale entries, unused
+          const int src = (gbase + off + u) & 63;
+          jj[u] = (uint32_t)bperm_i(src, wj);
+          bb[u] = bperm_f(src, wv);
+        }
         float dr[U][KV];
         float er[U][LV];
-        float bb[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           if (u < n) {
-            const int64_t j = bperm_i(gbase + off + u, wj);
-            bb[u] = bperm_f(gbase + off + u, wv);
-            if (MODE != kSpmm) ldv<KV>(dr[u], Dm + j * K + q * KV);
-            if (MODE != kSddmm) ldv<LV>(er[u], Em + j * L + glane * LV);
+            if (u > 0) wait_vmcnt<1>();
+            if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
+            if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
           }
         }
         float ysel = 0.f;
@@ -255,7 +384,7 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
         for (int u = 0; u < U; ++u) {
           if (u < n) {
             float y;
-            if (MODE == kSpmm) {
+            if constexpr (MODE == kSpmm) {
               y = bb[u];
             } else {
               float t = 0.f;
@@ -264,13 +393,61 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
               t = group_sum<W>(t);
               y = bb[u] * t;
             }
-            if (MODE == kSddmm) {
+            if constexpr (MODE == kSddmm) {
               if (glane == u) ysel = y;
             } else {
 #pragma unroll
               for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, er[u][v], acc[v]);
             }
           }
+        }
+        if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
+      } else if constexpr (NB == 1) {
+        // Depth-2 software pipeline: the gathers of nonzero u are in flight
+        // while nonzero u-1 is reduced and applied.  The loop body is
+        // straight-line, so the wait before each consume covers exactly the
+        // older pair of loads.
+        Gather<MODE, KV, LV> ga, gb;
+        float ysel = 0.f;
+        auto issue = [&](Gather<MODE, KV, LV> &g, int u) {
+          const int src = gbase + off + u;
+          const uint32_t j = (uint32_t)bperm_i(src, wj);
+          g.b = bperm_f(src, wv);
+          if constexpr (MODE != kSpmm) ldv_off<KV>(g.d, Dm, j * strideD + offD);
+          if constexpr (MODE != kSddmm) ldv_off<LV>(g.e, Em, j * strideE + offE);
+        };
+        auto consume = [&](const Gather<MODE, KV, LV> &g, int u) {
+          float y;
+          if constexpr (MODE == kSpmm) {
+            y = g.b;
+          } else {
+            float t = 0.f;
+#pragma unroll
+            for (int v = 0; v < KV; ++v) t = fmaf(c[v], g.d[v], t);
+            t = group_sum<W>(t);
+            y = g.b * t;
+          }
+          if constexpr (MODE == kSddmm) {
+            if (glane == u) ysel = y;
+          } else {
+#pragma unroll
+            for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v], acc[v]);
+          }
+        };
+        issue(ga, 0);
+        int u = 1;
+        for (; u + 1 < n; u += 2) {
+          issue(gb, u);
+          consume(ga, u - 1);
+          issue(ga, u + 1);
+          consume(gb, u);
+        }
+        if (u < n) {
+          issue(gb, u);
+          consume(ga, u - 1);
+          consume(gb, u);
+        } else {
+          consume(ga, u - 1);
         }
         if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
       } else {
@@ -280,12 +457,12 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
         if (MODE != kSpmm) {
           // (lanes with sub >= n read a stale window entry and discard it)
           const int src = (gbase + off + sub) & 63;
-          const int64_t js = bperm_i(src, wj);
+          const uint32_t js = (uint32_t)bperm_i(src, wj);
           const float bs = bperm_f(src, wv);
           float dr[KV];
           float t = 0.f;
           if (act) {
-            ldv<KV>(dr, Dm + js * K + q * KV);
+            ldv_off<KV>(dr, Dm, js * strideD + offD);
 #pragma unroll
             for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[v], t);
           }
@@ -293,34 +470,69 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
           y = bs * t;
           if (MODE == kSddmm && act && q == 0) out[p + sub] = y;
         }
-        if (MODE != kSddmm) {
-          float er[U][LV];
-          float yy[U];
+        if (MODE != kSddmm && SCHED == kPaced) {
+          // consumer: the whole worker streams each E row, one row issued
+          // after the previous one has arrived
+          uint32_t jj[NB];
+          float yy[NB];
 #pragma unroll
-          for (int u = 0; u < U; ++u) {
+          for (int u = 0; u < NB; ++u) {
+            const int src = (gbase + off + u) & 63;
+            jj[u] = (uint32_t)bperm_i(src, wj);
+            yy[u] = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f((gbase + u * PS) & 63, y);
+          }
+          float er[NB][LV];
+#pragma unroll
+          for (int u = 0; u < NB; ++u) {
             if (u < n) {
-              const int64_t j = bperm_i(gbase + off + u, wj);
-              yy[u] = (MODE == kSpmm) ? bperm_f(gbase + off + u, wv) : bperm_f(gbase + u * PS, y);
-              ldv<LV>(er[u], Em + j * L + glane * LV);
+              if (u > 0) wait_vmcnt<1>();
+              ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
             }
           }
 #pragma unroll
-          for (int u = 0; u < U; ++u) {
+          for (int u = 0; u < NB; ++u) {
             if (u < n) {
 #pragma unroll
               for (int v = 0; v < LV; ++v) acc[v] = fmaf(yy[u], er[u][v], acc[v]);
             }
+          }
+        } else if (MODE != kSddmm) {
+          // consumer: the whole worker streams each E row, depth-2 pipeline
+          float ea[LV], eb[LV];
+          float ya = 0.f, yb = 0.f;
+          auto issue = [&](float (&e)[LV], float &yv, int u) {
+            const int src = gbase + off + u;
+            const uint32_t j = (uint32_t)bperm_i(src, wj);
+            yv = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f(gbase + u * PS, y);
+            ldv_off<LV>(e, Em, j * strideE + offE);
+          };
+          auto consume = [&](const float (&e)[LV], float yv) {
+#pragma unroll
+            for (int v = 0; v < LV; ++v) acc[v] = fmaf(yv, e[v], acc[v]);
+          };
+          issue(ea, ya, 0);
+          int u = 1;
+          for (; u + 1 < n; u += 2) {
+            issue(eb, yb, u);
+            consume(ea, ya);
+            issue(ea, ya, u + 1);
+            consume(eb, yb);
+          }
+          if (u < n) {
+            issue(eb, yb, u);
+            consume(ea, ya);
+            consume(eb, yb);
+          } else {
+            consume(ea, ya);
           }
         }
       }
       p += n;
     }
     if (MODE != kSddmm) {
-      float *dst;
-      if (!has_end) dst = a.carry + (worker * 2 + 1) * (int64_t)a.Lw;
-      else if (i == s.i0 && s.head) dst = a.carry + (worker * 2) * (int64_t)a.Lw;
-      else dst = out + i * L;
-      stv<LV>(dst + glane * LV, acc);
+      if (!has_end) stv<LV>(a.carry + (worker * 2 + 1) * (int64_t)a.Lw + glane * LV, acc);
+      else if (i == s.i0 && s.head) stv<LV>(a.carry + (worker * 2) * (int64_t)a.Lw + glane * LV, acc);
+      else stv<LV, kNT>(out + i * L + glane * LV, acc);
     }
     if (!has_end) break;
     ++i;
@@ -339,14 +551,10 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
 template <int MODE, int LT>
 __global__ __launch_bounds__(256) void walk_generic(WalkArgs a) {
   const int lane = threadIdx.x & 63;
-  const int64_t worker = logical_block(a) * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (worker >= a.workers) return;
+  const Slice s = make_slice<64>(a);
+  if (!s.active) return;
+  const int64_t worker = s.id;  // carry slots and metadata are per slice
   int32_t *meta = a.meta + 2 * worker;
-  const Slice s = make_slice(a, worker);
-  if (!s.active) {
-    if (MODE != kSddmm && lane == 0) { meta[0] = -1; meta[1] = -1; }
-    return;
-  }
   const int32_t *__restrict__ rowptr = a.rowptr;
   const int64_t K = a.K, L = a.L, N = a.N, Lw = a.Lw, l0 = a.l0;
   int64_t i = s.i0, p = s.p0;
@@ -405,13 +613,16 @@ __global__ __launch_bounds__(256) void walk_generic(WalkArgs a) {
 // by earlier slices) adds, in slice order, the tail partials of the earlier
 // slices that end inside that row, then its own head partial, and writes
 // the row of A.
-__global__ __launch_bounds__(256) void carry_fixup(const float *__restrict__ carry,
-                                                   const int32_t *__restrict__ meta,
-                                                   float *__restrict__ A, int32_t workers,
-                                                   int32_t Lw, int32_t L, int32_t l0) {
+__global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
+  const float *__restrict__ carry = a.carry;
+  const int32_t *__restrict__ meta = a.meta;
+  float *__restrict__ A = a.out;
+  const int64_t Lw = a.Lw, L = a.L, l0 = a.l0;
   const int lane = threadIdx.x & 63;
   const int64_t c = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  if (c >= workers) return;
+  int64_t S, ns, items, nnz;
+  slice_count(a, &S, &ns, &items, &nnz);
+  if (c >= ns) return;
   const int32_t r = meta[2 * c + 1];
   if (r < 0) return;
   int64_t first = c;
@@ -423,9 +634,21 @@ __global__ __launch_bounds__(256) void carry_fixup(const float *__restrict__ car
     first -= run;
     if (run < 64) break;
   }
+  // Sum in slice order; the loads of a batch are issued together so a row
+  // split over hundreds of slices costs a few memory latencies, not one per
+  // slice.
+  constexpr int kBatch = 16;
   for (int64_t l = lane; l < Lw; l += 64) {
     float sum = 0.f;
-    for (int64_t cc = first; cc < c; ++cc) sum += carry[(cc * 2 + 1) * Lw + l];
+    int64_t cc = first;
+    for (; cc + kBatch <= c; cc += kBatch) {
+      float v[kBatch];
+#pragma unroll
+      for (int t = 0; t < kBatch; ++t) v[t] = carry[((cc + t) * 2 + 1) * Lw + l];
+#pragma unroll
+      for (int t = 0; t < kBatch; ++t) sum += v[t];
+    }
+    for (; cc < c; ++cc) sum += carry[(cc * 2 + 1) * Lw + l];
     sum += carry[(c * 2) * Lw + l];
     A[(int64_t)r * L + l0 + l] = sum;
   }

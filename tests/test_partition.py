@@ -132,3 +132,63 @@ def test_rows_ending_on_slice_boundaries():
         workers = -(-items // S)
         A, writes, consumed, ref = simulate(rowptr, workers, 1)
         assert np.all(consumed == 1) and np.all(writes == 1) and np.array_equal(A, ref)
+
+
+def mp_search_wide(rowptr, N, nnz, d, G):
+    """Host model of the kernel's G-lane search: G probes per step, keep the
+    sub-interval the ballot points to."""
+    lo, hi = max(0, d - nnz), min(d, N)
+    steps = 0
+    while lo < hi:
+        step = -(-(hi - lo) // G)
+        xs = [min(hi, lo + (t + 1) * step) for t in range(G)]
+        ok = [rowptr[x] + x <= d for x in xs]
+        m = 0
+        while m < G and ok[m]:
+            m += 1
+        assert all(ok[:m]) and not any(ok[m:]), "probe results must be monotone"
+        xm1, xm = lo + m * step, lo + (m + 1) * step
+        new_lo = min(xm1, hi) if m > 0 else lo
+        new_hi = min(xm, hi) - 1 if m < G else hi
+        lo, hi = new_lo, new_hi
+        steps += 1
+        assert steps < 64
+    return lo, steps
+
+
+@pytest.mark.parametrize("G", [4, 8, 16, 32, 64])
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_wide_search_matches_bisection(G, name):
+    rowptr = csr_from_lengths(CASES[name])
+    N, nnz = rowptr.size - 1, int(rowptr[-1])
+    for d in range(N + nnz + 1):
+        got, steps = mp_search_wide(rowptr, N, nnz, d, G)
+        assert got == mp_search(rowptr, N, nnz, d), (d, G)
+        assert rowptr[got] <= d - got <= (rowptr[got + 1] if got < N else nnz)
+
+
+def test_wide_search_step_count():
+    rowptr = csr_from_lengths([16] * (1 << 20))
+    N, nnz = rowptr.size - 1, int(rowptr[-1])
+    for d in [0, 1, 12345, N + nnz // 2, N + nnz]:
+        _, steps = mp_search_wide(rowptr, N, nnz, d, 32)
+        assert steps <= 5
+
+
+@pytest.mark.parametrize("blocks,wpb,ns", [(8, 8, 1), (8, 8, 64), (16, 2, 31), (24, 16, 383),
+                                           (64, 4, 256), (8, 1, 8), (40, 16, 7)])
+def test_xcd_slice_assignment_is_a_bijection(blocks, wpb, ns):
+    """XCD x (blocks dealt round-robin over 8 XCDs) takes slices
+    [x * ceil(ns/8), (x+1) * ceil(ns/8)); every slice < ns has one worker."""
+    xcds = 8
+    workers = blocks * wpb
+    assert ns <= workers
+    per_xcd = -(-ns // xcds)
+    seen = []
+    for b in range(blocks):
+        for local in range(wpb):
+            xcd, in_xcd = b % xcds, (b // xcds) * wpb + local
+            sid = xcd * per_xcd + in_xcd
+            if in_xcd < per_xcd and sid < ns:
+                seen.append(sid)
+    assert sorted(seen) == list(range(ns))
