@@ -267,6 +267,19 @@ __device__ __forceinline__ Slice make_slice(const WalkArgs &a) {
   s.p0 = d0 - s.i0;
   s.i1 = mp_search<W>(a.rowptr, a.N, nnz, d1);
   s.p1 = d1 - s.i1;
+  // A boundary inside a short row (at most S/4 nonzeros) moves back to the
+  // row's start, so only long rows are ever split between slices.  Both
+  // slices sharing the boundary apply the same rule, and the rule is
+  // monotone, so slices stay contiguous and ordered.
+  const int64_t snap = S / 4;
+  auto snap_back = [&](int64_t i, int64_t &p) {
+    if (i < a.N) {
+      const int64_t r0 = a.rowptr[i];
+      if (p > r0 && (int64_t)a.rowptr[i + 1] - r0 <= snap) p = r0;
+    }
+  };
+  snap_back(s.i0, s.p0);
+  snap_back(s.i1, s.p1);
   s.head = (s.i0 < s.i1) && (s.p0 > (int64_t)a.rowptr[s.i0]);
   return s;
 }
@@ -634,9 +647,9 @@ __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
     first -= run;
     if (run < 64) break;
   }
-  // Sum in slice order; the loads of a batch are issued together so a row
-  // split over hundreds of slices costs a few memory latencies, not one per
-  // slice.
+  // Sum in slice order.  The loads of a batch are issued together, so a row
+  // split over hundreds of slices (a power-law hub row) costs a few memory
+  // latencies rather than one per slice; the adds stay in slice order.
   constexpr int kBatch = 16;
   for (int64_t l = lane; l < Lw; l += 64) {
     float sum = 0.f;
@@ -648,7 +661,15 @@ __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
 #pragma unroll
       for (int t = 0; t < kBatch; ++t) sum += v[t];
     }
-    for (; cc < c; ++cc) sum += carry[(cc * 2 + 1) * Lw + l];
+    if (cc < c) {
+      float v[kBatch];
+#pragma unroll
+      for (int t = 0; t < kBatch; ++t)
+        if (cc + t < c) v[t] = carry[((cc + t) * 2 + 1) * Lw + l];
+#pragma unroll
+      for (int t = 0; t < kBatch; ++t)
+        if (cc + t < c) sum += v[t];
+    }
     sum += carry[(c * 2) * Lw + l];
     A[(int64_t)r * L + l0 + l] = sum;
   }

@@ -23,12 +23,23 @@ def mp_search(rowptr, N, nnz, d):
     return lo
 
 
-def simulate(rowptr, workers, min_chunk, L=3, rng=None):
+def slice_bounds(rowptr, N, nnz, S, d, snap):
+    """Merge-path coordinate of diagonal d, moved back to the row start when it
+    falls inside a row of at most `snap` nonzeros."""
+    i = mp_search(rowptr, N, nnz, d)
+    p = d - i
+    if i < N and p > rowptr[i] and rowptr[i + 1] - rowptr[i] <= snap:
+        p = int(rowptr[i])
+    return i, p
+
+
+def simulate(rowptr, workers, min_chunk, L=3, rng=None, use_snap=True):
     """Returns (A, writes) computed through the slice / carry / fixup rules."""
     N = rowptr.size - 1
     nnz = int(rowptr[N])
     items = N + nnz
     S = max(-(-items // workers), min_chunk)
+    snap = S // 4 if use_snap else -1
     rng = rng or np.random.default_rng(0)
     contrib = rng.integers(-5, 6, size=(nnz, L)).astype(np.float64)  # y_p * E_j, exact ints
     A = np.full((N, L), np.nan)
@@ -42,10 +53,8 @@ def simulate(rowptr, workers, min_chunk, L=3, rng=None):
             meta[w] = (-1, -1)
             continue
         d1 = min(d0 + S, items)
-        i0 = mp_search(rowptr, N, nnz, d0)
-        p0 = d0 - i0
-        i1 = mp_search(rowptr, N, nnz, d1)
-        p1 = d1 - i1
+        i0, p0 = slice_bounds(rowptr, N, nnz, S, d0, snap)
+        i1, p1 = slice_bounds(rowptr, N, nnz, S, d1, snap)
         assert 0 <= i0 <= i1 <= N and 0 <= p0 <= p1 <= nnz
         assert rowptr[i0] <= p0 <= (rowptr[i0 + 1] if i0 < N else nnz)
         head = i0 < i1 and p0 > rowptr[i0]
@@ -112,15 +121,28 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("use_snap", [True, False])
 @pytest.mark.parametrize("name", sorted(CASES))
 @pytest.mark.parametrize("workers,min_chunk", [(1, 1), (3, 1), (7, 2), (64, 1), (64, 32),
-                                                (1000, 1), (5, 1000)])
-def test_every_row_once(name, workers, min_chunk):
+                                                (1000, 1), (5, 1000), (40, 8)])
+def test_every_row_once(name, workers, min_chunk, use_snap):
     rowptr = csr_from_lengths(CASES[name])
-    A, writes, consumed, ref = simulate(rowptr, workers, min_chunk)
+    A, writes, consumed, ref = simulate(rowptr, workers, min_chunk, use_snap=use_snap)
     assert np.all(consumed == 1)
     assert np.all(writes == 1)
     assert np.array_equal(A, ref)
+
+
+def test_snapping_splits_only_long_rows():
+    lengths = [int(x) for x in (np.random.default_rng(2).pareto(1.2, 2000) * 3)]
+    rowptr = csr_from_lengths(lengths)
+    N, nnz = len(lengths), int(rowptr[-1])
+    workers = 300
+    S = max(-(-(N + nnz) // workers), 1)
+    for w in range(1, workers):
+        i, p = slice_bounds(rowptr, N, nnz, S, w * S, S // 4)
+        if i < N and p > rowptr[i]:
+            assert rowptr[i + 1] - rowptr[i] > S // 4
 
 
 def test_rows_ending_on_slice_boundaries():
@@ -130,8 +152,9 @@ def test_rows_ending_on_slice_boundaries():
         rowptr = csr_from_lengths(lengths)
         items = len(lengths) + rowptr[-1]
         workers = -(-items // S)
-        A, writes, consumed, ref = simulate(rowptr, workers, 1)
-        assert np.all(consumed == 1) and np.all(writes == 1) and np.array_equal(A, ref)
+        for use_snap in (True, False):
+            A, writes, consumed, ref = simulate(rowptr, workers, 1, use_snap=use_snap)
+            assert np.all(consumed == 1) and np.all(writes == 1) and np.array_equal(A, ref)
 
 
 def mp_search_wide(rowptr, N, nnz, d, G):
