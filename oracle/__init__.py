@@ -11,11 +11,17 @@ What it computes (oracle.c holds the loops):
 * ``fused_rows`` -- the result on chosen rows, each row computed as 2a then 2b
                     into a row-local value array, plus the per-row tolerance
                     scale  max_l sum_p |b_p| (sum_k |C_ik||D_jk|) |E_jl|.
+* ``sddmm_spmm_gemm_rows``, ``spmm_gemm_rows``, ``spmmh_gemm_rows`` -- the
+                    <SDDMM, SpMM, GEMM>, <SpMM, GEMM> and <SpMMH, GEMM>
+                    benchmarks of Section 6.2 on chosen rows (row of the sparse
+                    product, then times the dense matrix), with their scales.
+* ``fused_rows_dt`` -- <SDDMM, SpMM> with D stored transposed (Section 4.3.1).
 
 Pins that tie it to the paper and to mathematics (not to itself) are in
-tests/test_oracle.py: dense brute force A = (B .* C D^T) E, the perfect-nest
-form of Figure 2c, closed-form special cases, invariants and a hand-worked
-golden example.
+tests/test_oracle.py and tests/test_oracle_next.py: dense brute force
+A = (B .* C D^T) E (and the products of the other benchmarks), the
+perfect-nest form of Figure 2c, closed-form special cases, invariants and a
+hand-worked golden example.
 """
 from __future__ import annotations
 
@@ -133,3 +139,93 @@ def fused_rows(rowptr, colidx, vals, C, D, E, rows=None, with_y: bool = False):
     if with_y:
         return A, scale, Y, Ys, ops
     return A, scale, ops
+
+
+# ---------------------------------------------------------------- next rows
+
+def _rows(rows, N):
+    if rows is None:
+        rows = np.arange(N, dtype=np.int64)
+    return _c(rows, np.int64)
+
+
+def _setup_next():
+    L = lib()
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    if not hasattr(L, "_next_ready"):
+        L.oracle_sddmm_spmm_gemm_rows.restype = i64
+        L.oracle_sddmm_spmm_gemm_rows.argtypes = [i64, i64, i64] + [vp] * 7 + [vp, i64, vp, vp]
+        L.oracle_spmm_gemm_rows.restype = i64
+        L.oracle_spmm_gemm_rows.argtypes = [i64, i64] + [vp] * 5 + [vp, i64, vp, vp]
+        L.oracle_spmmh_gemm_rows.restype = i64
+        L.oracle_spmmh_gemm_rows.argtypes = [i64, i64] + [vp] * 6 + [vp, i64, vp, vp]
+        L.oracle_fused_rows_dt.restype = i64
+        L.oracle_fused_rows_dt.argtypes = [i64, i64, i64] + [vp] * 6 + [vp, i64, vp, vp]
+        L._next_ready = True
+    return L
+
+
+def sddmm_spmm_gemm_rows(rowptr, colidx, vals, C, D, F, W, rows=None):
+    """<SDDMM, SpMM, GEMM> (Section 6.2): A = ((B .* C D^T) F) W on the chosen
+    rows, in the fused loop order (row of <SDDMM, SpMM>, then times W)."""
+    rowptr, colidx, vals = _csr(rowptr, colidx, vals)
+    C, D, F, W = (_c(x, np.float32) for x in (C, D, F, W))
+    N, K = C.shape
+    L, Mo = W.shape
+    assert F.shape[1] == L and D.shape[1] == K
+    rows = _rows(rows, N)
+    out = np.empty((rows.size, Mo), np.float64)
+    scale = np.empty(rows.size, np.float64)
+    ops = _setup_next().oracle_sddmm_spmm_gemm_rows(K, L, Mo, _p(rowptr), _p(colidx), _p(vals),
+                                                   _p(C), _p(D), _p(F), _p(W), _p(rows),
+                                                   rows.size, _p(out), _p(scale))
+    return out, scale, ops
+
+
+def spmm_gemm_rows(rowptr, colidx, vals, C, D, rows=None):
+    """<SpMM, GEMM> (Section 6.2): A = (B C) D on the chosen rows; C is M x K,
+    D is K x L."""
+    rowptr, colidx, vals = _csr(rowptr, colidx, vals)
+    C, D = _c(C, np.float32), _c(D, np.float32)
+    K, L = D.shape
+    assert C.shape[1] == K
+    N = rowptr.size - 1
+    rows = _rows(rows, N)
+    out = np.empty((rows.size, L), np.float64)
+    scale = np.empty(rows.size, np.float64)
+    ops = _setup_next().oracle_spmm_gemm_rows(K, L, _p(rowptr), _p(colidx), _p(vals), _p(C),
+                                              _p(D), _p(rows), rows.size, _p(out), _p(scale))
+    return out, scale, ops
+
+
+def spmmh_gemm_rows(rowptr, colidx, vals, C, D, E, rows=None):
+    """<SpMMH, GEMM> (Section 6.2): A = (B (C .* D)) E on the chosen rows;
+    C, D are M x J, E is J x L."""
+    rowptr, colidx, vals = _csr(rowptr, colidx, vals)
+    C, D, E = (_c(x, np.float32) for x in (C, D, E))
+    J, L = E.shape
+    assert C.shape[1] == J and D.shape == C.shape
+    N = rowptr.size - 1
+    rows = _rows(rows, N)
+    out = np.empty((rows.size, L), np.float64)
+    scale = np.empty(rows.size, np.float64)
+    ops = _setup_next().oracle_spmmh_gemm_rows(J, L, _p(rowptr), _p(colidx), _p(vals), _p(C),
+                                               _p(D), _p(E), _p(rows), rows.size, _p(out),
+                                               _p(scale))
+    return out, scale, ops
+
+
+def fused_rows_dt(rowptr, colidx, vals, C, Dt, E, rows=None):
+    """<SDDMM, SpMM> with D stored transposed (Dt is K x M; Section 4.3.1)."""
+    rowptr, colidx, vals = _csr(rowptr, colidx, vals)
+    C, Dt, E = (_c(x, np.float32) for x in (C, Dt, E))
+    N, K = C.shape
+    M, L = E.shape
+    assert Dt.shape == (K, M)
+    rows = _rows(rows, N)
+    out = np.empty((rows.size, L), np.float64)
+    scale = np.empty(rows.size, np.float64)
+    ops = _setup_next().oracle_fused_rows_dt(M, K, L, _p(rowptr), _p(colidx), _p(vals), _p(C),
+                                             _p(Dt), _p(E), _p(rows), rows.size, _p(out),
+                                             _p(scale))
+    return out, scale, ops

@@ -179,3 +179,206 @@ int64_t oracle_fused_rows(int64_t N, int64_t M, int64_t K, int64_t L,
   free(yoff);
   return ops;
 }
+
+/* ------------------------------------------------------------------------
+ * Further computations of the paper's Section 6.2 benchmarks, each written
+ * in its fused loop order on the chosen rows, fp64, with the abs-value scale
+ * of the result (the same loops on |.|).  out is nrows x (output width).
+ */
+
+/* Scratch of one thread: two vectors of length n. */
+static int ensure(double **a, double **b, int64_t *cap, int64_t n) {
+  if (n <= *cap) return 0;
+  *a = (double *)realloc(*a, sizeof(double) * (size_t)n);
+  *b = (double *)realloc(*b, sizeof(double) * (size_t)n);
+  *cap = n;
+  return (*a && *b) ? 0 : 1;
+}
+
+/* <SDDMM, SpMM, GEMM>: A(i,m) = sum_{j,k,l} B(i,j) C(i,k) D(j,k) F(j,l) W(l,m).
+ * Per row: t_l = sum_p b_p (sum_k C_ik D_jk) F_jl (the <SDDMM, SpMM> row),
+ * then A_im = sum_l t_l W_lm.  C: N x K, D: M x K, F: M x L, W: L x Mo. */
+int64_t oracle_sddmm_spmm_gemm_rows(int64_t K, int64_t L, int64_t Mo, const int32_t *rowptr,
+                                    const int32_t *colidx, const float *vals, const float *C,
+                                    const float *D, const float *F, const float *Wm,
+                                    const int64_t *rows, int64_t nrows, double *out,
+                                    double *scale_out) {
+  int64_t ops = 0;
+#pragma omp parallel reduction(+ : ops)
+  {
+    double *t = NULL, *ta = NULL;
+    int64_t cap = 0;
+    ensure(&t, &ta, &cap, L > 0 ? L : 1);
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t i = rows[r];
+      for (int64_t l = 0; l < L; ++l) { t[l] = 0.0; ta[l] = 0.0; }
+      for (int64_t p = rowptr[i]; p < rowptr[i + 1]; ++p) {
+        const int64_t j = colidx[p];
+        double dot = 0.0, adot = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+          const double c = (double)C[i * K + k], d = (double)D[j * K + k];
+          dot += c * d;
+          adot += fabs(c) * fabs(d);
+          ++ops;
+        }
+        const double y = (double)vals[p] * dot, ya = fabs((double)vals[p]) * adot;
+        for (int64_t l = 0; l < L; ++l) {
+          t[l] += y * (double)F[j * L + l];
+          ta[l] += ya * fabs((double)F[j * L + l]);
+          ++ops;
+        }
+      }
+      double m_scale = 0.0;
+      for (int64_t m = 0; m < Mo; ++m) {
+        double s = 0.0, sa = 0.0;
+        for (int64_t l = 0; l < L; ++l) {
+          s += t[l] * (double)Wm[l * Mo + m];
+          sa += ta[l] * fabs((double)Wm[l * Mo + m]);
+          ++ops;
+        }
+        out[r * Mo + m] = s;
+        m_scale = sa > m_scale ? sa : m_scale;
+      }
+      scale_out[r] = m_scale;
+    }
+    free(t);
+    free(ta);
+  }
+  return ops;
+}
+
+/* <SpMM, GEMM>: A(i,l) = sum_{j,k} B(i,j) C(j,k) D(k,l).  Per row: the SpMM
+ * row t_k = sum_p b_p C_jk, then A_il = sum_k t_k D_kl.  C: M x K, D: K x L. */
+int64_t oracle_spmm_gemm_rows(int64_t K, int64_t L, const int32_t *rowptr,
+                              const int32_t *colidx, const float *vals, const float *C,
+                              const float *D, const int64_t *rows, int64_t nrows, double *out,
+                              double *scale_out) {
+  int64_t ops = 0;
+#pragma omp parallel reduction(+ : ops)
+  {
+    double *t = NULL, *ta = NULL;
+    int64_t cap = 0;
+    ensure(&t, &ta, &cap, K > 0 ? K : 1);
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t i = rows[r];
+      for (int64_t k = 0; k < K; ++k) { t[k] = 0.0; ta[k] = 0.0; }
+      for (int64_t p = rowptr[i]; p < rowptr[i + 1]; ++p) {
+        const int64_t j = colidx[p];
+        const double b = (double)vals[p];
+        for (int64_t k = 0; k < K; ++k) {
+          t[k] += b * (double)C[j * K + k];
+          ta[k] += fabs(b) * fabs((double)C[j * K + k]);
+          ++ops;
+        }
+      }
+      double m_scale = 0.0;
+      for (int64_t l = 0; l < L; ++l) {
+        double s = 0.0, sa = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+          s += t[k] * (double)D[k * L + l];
+          sa += ta[k] * fabs((double)D[k * L + l]);
+          ++ops;
+        }
+        out[r * L + l] = s;
+        m_scale = sa > m_scale ? sa : m_scale;
+      }
+      scale_out[r] = m_scale;
+    }
+    free(t);
+    free(ta);
+  }
+  return ops;
+}
+
+/* <SpMMH, GEMM>: A(i,l) = sum_{k,j} B(i,k) C(k,j) D(k,j) E(j,l).  Per row: the
+ * Hadamard SpMM row t_j = sum_p b_p C_kj D_kj (k = colidx[p]), then
+ * A_il = sum_j t_j E_jl.  C, D: M x J, E: J x L. */
+int64_t oracle_spmmh_gemm_rows(int64_t J, int64_t L, const int32_t *rowptr,
+                               const int32_t *colidx, const float *vals, const float *C,
+                               const float *D, const float *E, const int64_t *rows,
+                               int64_t nrows, double *out, double *scale_out) {
+  int64_t ops = 0;
+#pragma omp parallel reduction(+ : ops)
+  {
+    double *t = NULL, *ta = NULL;
+    int64_t cap = 0;
+    ensure(&t, &ta, &cap, J > 0 ? J : 1);
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t i = rows[r];
+      for (int64_t jj = 0; jj < J; ++jj) { t[jj] = 0.0; ta[jj] = 0.0; }
+      for (int64_t p = rowptr[i]; p < rowptr[i + 1]; ++p) {
+        const int64_t k = colidx[p];
+        const double b = (double)vals[p];
+        for (int64_t jj = 0; jj < J; ++jj) {
+          const double c = (double)C[k * J + jj], d = (double)D[k * J + jj];
+          t[jj] += b * c * d;
+          ta[jj] += fabs(b) * fabs(c) * fabs(d);
+          ++ops;
+        }
+      }
+      double m_scale = 0.0;
+      for (int64_t l = 0; l < L; ++l) {
+        double s = 0.0, sa = 0.0;
+        for (int64_t jj = 0; jj < J; ++jj) {
+          s += t[jj] * (double)E[jj * L + l];
+          sa += ta[jj] * fabs((double)E[jj * L + l]);
+          ++ops;
+        }
+        out[r * L + l] = s;
+        m_scale = sa > m_scale ? sa : m_scale;
+      }
+      scale_out[r] = m_scale;
+    }
+    free(t);
+    free(ta);
+  }
+  return ops;
+}
+
+/* <SDDMM, SpMM> with D stored transposed (Section 4.3.1): Dt is K x M and
+ * D(j,k) is read as Dt[k*M + j].  Otherwise as oracle_fused_rows. */
+int64_t oracle_fused_rows_dt(int64_t M, int64_t K, int64_t L, const int32_t *rowptr,
+                             const int32_t *colidx, const float *vals, const float *C,
+                             const float *Dt, const float *E, const int64_t *rows,
+                             int64_t nrows, double *out, double *scale_out) {
+  int64_t ops = 0;
+#pragma omp parallel reduction(+ : ops)
+  {
+    double *t = NULL, *ta = NULL;
+    int64_t cap = 0;
+    ensure(&t, &ta, &cap, L > 0 ? L : 1);
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t r = 0; r < nrows; ++r) {
+      const int64_t i = rows[r];
+      for (int64_t l = 0; l < L; ++l) { t[l] = 0.0; ta[l] = 0.0; }
+      for (int64_t p = rowptr[i]; p < rowptr[i + 1]; ++p) {
+        const int64_t j = colidx[p];
+        double dot = 0.0, adot = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+          const double c = (double)C[i * K + k], d = (double)Dt[k * M + j];
+          dot += c * d;
+          adot += fabs(c) * fabs(d);
+          ++ops;
+        }
+        const double y = (double)vals[p] * dot, ya = fabs((double)vals[p]) * adot;
+        for (int64_t l = 0; l < L; ++l) {
+          t[l] += y * (double)E[j * L + l];
+          ta[l] += ya * fabs((double)E[j * L + l]);
+          ++ops;
+        }
+      }
+      double m_scale = 0.0;
+      for (int64_t l = 0; l < L; ++l) {
+        out[r * L + l] = t[l];
+        m_scale = ta[l] > m_scale ? ta[l] : m_scale;
+      }
+      scale_out[r] = m_scale;
+    }
+    free(t);
+    free(ta);
+  }
+  return ops;
+}
