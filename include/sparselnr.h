@@ -59,6 +59,12 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#if defined(__GNUC__)
+#define SPARSELNR_API __attribute__((visibility("default")))
+#else
+#define SPARSELNR_API
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -78,7 +84,7 @@ enum sparselnr_status_code {
 #define SPARSELNR_MAX_WIDTH 65536
 
 /* Version of this interface (incremented on incompatible change). */
-int sparselnr_abi_version(void);
+SPARSELNR_API int sparselnr_abi_version(void);
 
 /*
  * Fused SDDMM->SpMM (Figure 2d; Section 3.1.3):
@@ -87,7 +93,7 @@ int sparselnr_abi_version(void);
  * k-reduction done as a lane-parallel tree and the l-update accumulated in
  * nonzero order.  Needs the per-(device, stream) workspace.
  */
-int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+SPARSELNR_API int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
                                const float *vals, const float *C,
                                const float *D, const float *E, float *A,
                                int64_t N, int64_t M, int64_t K, int64_t L,
@@ -98,22 +104,80 @@ int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
  * writes Y (nnz floats, structure of B, same order as colidx), then the SpMM
  * reads it.  Same result as the fused call up to rounding order.
  */
-int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
+SPARSELNR_API int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
                                  const float *vals, const float *C,
                                  const float *D, const float *E, float *Y,
                                  float *A, int64_t N, int64_t M, int64_t K,
                                  int64_t L, void *stream);
 
 /* SDDMM alone (Figure 2a): Y[p] = vals[p] * dot(C(i,:), D(colidx[p],:)). */
-int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx,
+SPARSELNR_API int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx,
                     const float *vals, const float *C, const float *D,
                     float *Y, int64_t N, int64_t M, int64_t K, void *stream);
 
 /* SpMM alone (Figure 2b): A(i,:) = sum_{p in row i} Y[p] * E(colidx[p],:).
  * A is overwritten.  Needs the per-(device, stream) workspace. */
-int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
+SPARSELNR_API int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
                    const float *Y, const float *E, float *A, int64_t N,
                    int64_t M, int64_t L, void *stream);
+
+/*
+ * <SDDMM, SpMM, GEMM> (Section 6.2; the recursive application of the fusion
+ * in Section 4.2):
+ *   A(i,m) = sum_{j,k,l} B(i,j) C(i,k) D(j,k) F(j,l) W(l,m)
+ * computed as the fused <SDDMM, SpMM> row t_i (Figure 2d) followed, in the
+ * same pass, by the per-row product A_i = t_i W, so neither the nnz-sized
+ * SDDMM values nor the N x L matrix t is ever stored.
+ *   C: N x K, D: M x K, F: M x L, W: L x Mo, A: N x Mo (overwritten).
+ * Supported: K == L in {32, 64, 128} and Mo in {L/2, L}; 16-byte aligned
+ * operands.  Other shapes return SPARSELNR_ERR_UNSUPPORTED.
+ */
+SPARSELNR_API int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
+                                    const float *vals, const float *C,
+                                    const float *D, const float *F,
+                                    const float *W, float *A, int64_t N,
+                                    int64_t M, int64_t K, int64_t L, int64_t Mo,
+                                    void *stream);
+
+/*
+ * <SpMM, GEMM> (Section 6.2; the GNN hidden-state update):
+ *   A(i,l) = sum_{j,k} B(i,j) C(j,k) D(k,l)
+ * computed per row as the SpMM row t_i = sum_j B(i,j) C(j,:) (a vector
+ * temporary of length K, Section 6.3) followed by A_i = t_i D.
+ *   C: M x K, D: K x L, A: N x L (overwritten).
+ * Supported: K in {32, 64, 128} and L in {K/2, K}; 16-byte aligned operands.
+ */
+SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
+                        const float *vals, const float *C, const float *D,
+                        float *A, int64_t N, int64_t M, int64_t K, int64_t L,
+                        void *stream);
+
+/*
+ * <SpMMH, GEMM> (Section 6.2):
+ *   A(i,l) = sum_{k,j} B(i,k) C(k,j) D(k,j) E(j,l)
+ * computed per row as t_i = sum_k B(i,k) (C(k,:) .* D(k,:)) (length J)
+ * followed by A_i = t_i E.  B is N x M; C, D: M x J; E: J x L; A: N x L.
+ * Supported: J in {32, 64, 128} and L in {J/2, J}; 16-byte aligned operands.
+ */
+SPARSELNR_API int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx,
+                         const float *vals, const float *C, const float *D,
+                         const float *E, float *A, int64_t N, int64_t M,
+                         int64_t J, int64_t L, void *stream);
+
+/*
+ * <SDDMM, SpMM> with D stored transposed (Section 4.3.1: the layout whose
+ * temporary becomes a vector over j unless the loops are reordered):
+ *   A(i,l) = sum_{j,k} B(i,j) C(i,k) Dt(k,j) E(j,l),   Dt: K x M.
+ * On the GPU the reorder is done on the data: Dt is transposed once into a
+ * per-(device, stream) workspace of M x K floats (coalesced tile transpose),
+ * then the fused kernel runs.  Same result, shapes and errors as
+ * sparselnr_fused_sddmm_spmm; the workspace is freed by sparselnr_release().
+ */
+SPARSELNR_API int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,
+                                  const float *vals, const float *C,
+                                  const float *Dt, const float *E, float *A,
+                                  int64_t N, int64_t M, int64_t K, int64_t L,
+                                  void *stream);
 
 /*
  * Checks the CSR preconditions on the device: rowptr[0] == 0, rowptr
@@ -124,20 +188,20 @@ int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
  * nnz = rowptr[N] to *nnz_out (host pointer, may be NULL).
  * Returns SPARSELNR_OK or SPARSELNR_ERR_INVALID_CSR (or an error code).
  */
-int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx,
+SPARSELNR_API int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx,
                            int64_t N, int64_t M, int64_t colidx_len,
                            int64_t *nnz_out, void *stream);
 
 /* Static text for a status code (never NULL). */
-const char *sparselnr_status_string(int status);
+SPARSELNR_API const char *sparselnr_status_string(int status);
 
 /* hipError_t of the last failing HIP call made by this library on the
  * calling thread (0 if none). */
-int sparselnr_last_hip_error(void);
+SPARSELNR_API int sparselnr_last_hip_error(void);
 
 /* Waits for the device(s) and frees every workspace the library allocated.
  * Safe to call at any time; later calls allocate again. */
-int sparselnr_release(void);
+SPARSELNR_API int sparselnr_release(void);
 
 #ifdef __cplusplus
 } /* extern "C" */

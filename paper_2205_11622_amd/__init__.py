@@ -23,7 +23,8 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_INVALID_CSR = 
 
 __all__ = [
     "sparselnr_fused_sddmm_spmm", "sparselnr_unfused_sddmm_spmm", "sparselnr_sddmm",
-    "sparselnr_spmm", "sparselnr_validate_csr", "sparselnr_release", "sparselnr_status_string",
+    "sparselnr_spmm", "sparselnr_fused_sddmm_spmm_gemm", "sparselnr_spmm_gemm",
+    "sparselnr_spmmh_gemm", "sparselnr_fused_sddmm_spmm_dt", "sparselnr_validate_csr", "sparselnr_release", "sparselnr_status_string",
     "sparselnr_last_hip_error", "sparselnr_abi_version", "SparseLNRError", "lib", "LIB_PATH",
 ]
 
@@ -57,6 +58,14 @@ def lib() -> ctypes.CDLL:
         L.sparselnr_sddmm.restype = ci
         L.sparselnr_spmm.argtypes = [vp] * 5 + [i64] * 3 + [vp]
         L.sparselnr_spmm.restype = ci
+        L.sparselnr_fused_sddmm_spmm_gemm.argtypes = [vp] * 8 + [i64] * 5 + [vp]
+        L.sparselnr_fused_sddmm_spmm_gemm.restype = ci
+        L.sparselnr_spmm_gemm.argtypes = [vp] * 6 + [i64] * 4 + [vp]
+        L.sparselnr_spmm_gemm.restype = ci
+        L.sparselnr_spmmh_gemm.argtypes = [vp] * 7 + [i64] * 4 + [vp]
+        L.sparselnr_spmmh_gemm.restype = ci
+        L.sparselnr_fused_sddmm_spmm_dt.argtypes = [vp] * 7 + [i64] * 4 + [vp]
+        L.sparselnr_fused_sddmm_spmm_dt.restype = ci
         L.sparselnr_validate_csr.argtypes = [vp, vp, i64, i64, i64, ctypes.POINTER(i64), vp]
         L.sparselnr_validate_csr.restype = ci
         L.sparselnr_status_string.argtypes = [ci]
@@ -243,6 +252,89 @@ def sparselnr_unfused_sddmm_spmm(rowptr, colidx, vals, C, D, E, Y=None, A=None, 
     if rc != OK:
         raise SparseLNRError(rc, "sparselnr_unfused_sddmm_spmm")
     return Y, A
+
+
+def _out(A, rows, cols, device, name="A"):
+    torch = _torch()
+    if A is None:
+        return torch.empty((rows, cols), dtype=torch.float32, device=device)
+    if _dense(A, name, rows, device) != cols:
+        raise ValueError("%s must be %d x %d" % (name, rows, cols))
+    return A
+
+
+def sparselnr_fused_sddmm_spmm_gemm(rowptr, colidx, vals, C, D, F, W, A=None, stream=None):
+    """<SDDMM, SpMM, GEMM>: A = ((B .* C D^T) F) W, one pass (Section 6.2).
+    C: N x K, D: M x K, F: M x L, W: L x Mo.  Returns A (N x Mo)."""
+    torch = _torch()
+    device, N = _csr(rowptr, colidx, vals)
+    K = _dense(C, "C", N, device)
+    M = D.shape[0] if isinstance(D, torch.Tensor) and D.dim() == 2 else -1
+    if _dense(D, "D", M, device) != K:
+        raise ValueError("C and D differ in width K")
+    L = _dense(F, "F", M, device)
+    Mo = _dense(W, "W", L, device)
+    A = _out(A, N, Mo, device)
+    rc = lib().sparselnr_fused_sddmm_spmm_gemm(
+        _ptr(rowptr, device), _ptr(colidx, device), _ptr(vals, device), _ptr(C, device),
+        _ptr(D, device), _ptr(F, device), _ptr(W, device), _ptr(A, device), N, M, K, L, Mo,
+        _stream(stream, device))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_fused_sddmm_spmm_gemm")
+    return A
+
+
+def sparselnr_spmm_gemm(rowptr, colidx, vals, C, D, A=None, stream=None):
+    """<SpMM, GEMM>: A = (B C) D (Section 6.2).  C: M x K, D: K x L.  Returns A (N x L)."""
+    torch = _torch()
+    device, N = _csr(rowptr, colidx, vals)
+    M = C.shape[0] if isinstance(C, torch.Tensor) and C.dim() == 2 else -1
+    K = _dense(C, "C", M, device)
+    L = _dense(D, "D", K, device)
+    A = _out(A, N, L, device)
+    rc = lib().sparselnr_spmm_gemm(_ptr(rowptr, device), _ptr(colidx, device),
+                                   _ptr(vals, device), _ptr(C, device), _ptr(D, device),
+                                   _ptr(A, device), N, M, K, L, _stream(stream, device))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_spmm_gemm")
+    return A
+
+
+def sparselnr_spmmh_gemm(rowptr, colidx, vals, C, D, E, A=None, stream=None):
+    """<SpMMH, GEMM>: A = (B (C .* D)) E (Section 6.2).  C, D: M x J, E: J x L."""
+    torch = _torch()
+    device, N = _csr(rowptr, colidx, vals)
+    M = C.shape[0] if isinstance(C, torch.Tensor) and C.dim() == 2 else -1
+    J = _dense(C, "C", M, device)
+    if _dense(D, "D", M, device) != J:
+        raise ValueError("C and D must have the same shape")
+    L = _dense(E, "E", J, device)
+    A = _out(A, N, L, device)
+    rc = lib().sparselnr_spmmh_gemm(_ptr(rowptr, device), _ptr(colidx, device),
+                                    _ptr(vals, device), _ptr(C, device), _ptr(D, device),
+                                    _ptr(E, device), _ptr(A, device), N, M, J, L,
+                                    _stream(stream, device))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_spmmh_gemm")
+    return A
+
+
+def sparselnr_fused_sddmm_spmm_dt(rowptr, colidx, vals, C, Dt, E, A=None, stream=None):
+    """<SDDMM, SpMM> with D stored transposed (Dt: K x M, Section 4.3.1)."""
+    torch = _torch()
+    device, N = _csr(rowptr, colidx, vals)
+    K = _dense(C, "C", N, device)
+    M = E.shape[0] if isinstance(E, torch.Tensor) and E.dim() == 2 else -1
+    if _dense(Dt, "Dt", K, device) != M:
+        raise ValueError("Dt must be K x M")
+    L = _dense(E, "E", M, device)
+    A = _out(A, N, L, device)
+    rc = lib().sparselnr_fused_sddmm_spmm_dt(
+        _ptr(rowptr, device), _ptr(colidx, device), _ptr(vals, device), _ptr(C, device),
+        _ptr(Dt, device), _ptr(E, device), _ptr(A, device), N, M, K, L, _stream(stream, device))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_fused_sddmm_spmm_dt")
+    return A
 
 
 def sparselnr_validate_csr(rowptr, colidx, M, stream=None) -> int:

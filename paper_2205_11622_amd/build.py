@@ -30,7 +30,7 @@ def hipcc() -> str:
 def flags() -> list:
     return ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-Wall", "-Wno-unused-result", "-I", INCLUDE, "-I", CSRC]
+            "-fvisibility=hidden", "-Wall", "-Wno-unused-result", "-I", INCLUDE, "-I", CSRC]
 
 
 def build(verbose: bool = False) -> str:

@@ -47,7 +47,19 @@ std::mutex g_mu;
 std::map<int, int> g_cus;                                    // device -> CUs
 std::map<std::pair<int, uintptr_t>, int> g_occupancy;        // (device, kernel) -> blocks/CU
 int g_grid_factor = 0;  // resident grids per launch (SPARSELNR_GRID_FACTOR; -1: by size)
-std::map<std::pair<int, uintptr_t>, Workspace> g_workspace;  // (device, stream)
+// workspaces per (device, stream, slot): slot 0 carry partials, slot 1 the
+// transposed D of the transposed-D entry point
+struct WsKey {
+  int dev;
+  uintptr_t stream;
+  int slot;
+  bool operator<(const WsKey &o) const {
+    if (dev != o.dev) return dev < o.dev;
+    if (stream != o.stream) return stream < o.stream;
+    return slot < o.slot;
+  }
+};
+std::map<WsKey, Workspace> g_workspace;
 
 int current_device(int *dev) {
   hipError_t e = hipGetDevice(dev);
@@ -73,9 +85,9 @@ int device_cus(int dev, int *cus) {
 
 // Workspace of at least `bytes` for (device, stream); grows by reallocation
 // after the stream has drained (only on the first calls of a new shape).
-int get_workspace(int dev, hipStream_t stream, size_t bytes, void **out) {
+int get_workspace(int dev, hipStream_t stream, size_t bytes, void **out, int slot = 0) {
   std::lock_guard<std::mutex> lock(g_mu);
-  Workspace &w = g_workspace[{dev, (uintptr_t)stream}];
+  Workspace &w = g_workspace[WsKey{dev, (uintptr_t)stream, slot}];
   if (w.bytes < bytes) {
     if (w.ptr) {
       hipError_t e = hipStreamSynchronize(stream);
@@ -114,14 +126,17 @@ struct Variant {
   KernelFn fn = nullptr;
   int W = 64;          // lanes per worker
   bool generic = true; // generic kernel (l-tiles of 256 columns)
+  size_t lds = 0;      // dynamic LDS bytes per block (epilogue matrix + row slots)
 };
 
-template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1>
+template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1,
+          int HAD = 0, int LVO = 0>
 Variant fast() {
   Variant v;
-  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, SCHED, U>;
+  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, SCHED, U, HAD, LVO>;
   v.W = W;
   v.generic = false;
+  if (LVO > 0) v.lds = sizeof(float) * (size_t)W * LV * W * LVO;  // the epilogue matrix
   return v;
 }
 
@@ -190,6 +205,23 @@ Variant pick_spmm(int64_t L, bool al) {
   return generic<kSpmm>();
 }
 
+// Section 6.2 benchmarks with a per-row epilogue (pipelined schedule).  The
+// consumer rows are W * 4 wide; the stored rows W * LVO (LVO = 2 or 4).
+template <int MODE, int W, int HAD>
+Variant pick_epi_lvo(int64_t Lout) {
+  if (Lout == 2 * W) return fast<MODE, W, 1, 4, 4, slnr::kPipelined, 1, HAD, 2>();
+  if (Lout == 4 * W) return fast<MODE, W, 1, 4, 4, slnr::kPipelined, 1, HAD, 4>();
+  return Variant{};
+}
+
+template <int MODE, int HAD>
+Variant pick_epi(int64_t Lin, int64_t Lout) {
+  if (Lin == 32) return pick_epi_lvo<MODE, 8, HAD>(Lout);
+  if (Lin == 64) return pick_epi_lvo<MODE, 16, HAD>(Lout);
+  if (Lin == 128) return pick_epi_lvo<MODE, 32, HAD>(Lout);
+  return Variant{};
+}
+
 struct Grid {
   int blocks;
   int workers;
@@ -197,7 +229,7 @@ struct Grid {
 };
 
 // Resident blocks per CU for `fn` (occupancy query, cached per device).
-int blocks_per_cu(int dev, KernelFn fn, int *out) {
+int blocks_per_cu(int dev, KernelFn fn, size_t lds, int *out) {
   std::lock_guard<std::mutex> lock(g_mu);
   if (g_grid_factor == 0) {
     const char *env = getenv("SPARSELNR_GRID_FACTOR");
@@ -211,7 +243,7 @@ int blocks_per_cu(int dev, KernelFn fn, int *out) {
     return SPARSELNR_OK;
   }
   int nb = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)fn, kBlock, 0);
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)fn, kBlock, lds);
   if (e != hipSuccess) return hip_fail(e);
   if (nb <= 0) nb = 1;
   g_occupancy[key] = nb;
@@ -245,7 +277,7 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
   if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
   if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
   int per_cu = 1;
-  if ((rc = blocks_per_cu(dev, v.fn, &per_cu)) != SPARSELNR_OK) return rc;
+  if ((rc = blocks_per_cu(dev, v.fn, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
   const Grid g = make_grid(cus, per_cu, v.W, a.N);
   a.workers = g.workers;
   a.min_chunk = kMinChunk;
@@ -268,7 +300,7 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
   for (int64_t t = 0; t < (mode == kSddmm ? 1 : tiles); ++t) {
     a.l0 = (int32_t)(t * tile_w);
     a.Lw = (int32_t)((a.L - a.l0) < tile_w ? (a.L - a.l0) : tile_w);
-    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(kBlock), 0, stream, a);
+    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(kBlock), v.lds, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e);
     if (mode != kSddmm) {
@@ -302,7 +334,29 @@ WalkArgs base_args(const int32_t *rowptr, const int32_t *colidx, const float *va
   a.L = (int32_t)L;
   a.l0 = 0;
   a.Lw = (int32_t)L;
+  a.Lin = (int32_t)L;
+  a.G2 = nullptr;
+  a.Wep = nullptr;
   return a;
+}
+
+// Shared driver of the epilogue entry points.
+int run_epilogue(Mode mode, bool had, const int32_t *rowptr, const int32_t *colidx,
+                 const float *vals, const float *C, const float *D, const float *E,
+                 const float *G2, const float *Wm, float *A, int64_t N, int64_t Kdot,
+                 int64_t Lin, int64_t Lout, void *stream) {
+  Variant v = mode == kFused ? pick_epi<kFused, 0>(Lin, Lout)
+                             : (had ? pick_epi<kSpmm, 1>(Lin, Lout) : pick_epi<kSpmm, 0>(Lin, Lout));
+  if (!v.fn) return SPARSELNR_ERR_UNSUPPORTED;
+  WalkArgs a = base_args(rowptr, colidx, vals, N, Kdot, Lout);
+  a.C = C;
+  a.D = D;
+  a.E = E;
+  a.G2 = G2;
+  a.Wep = Wm;
+  a.Lin = (int32_t)Lin;
+  a.out = A;
+  return run_walk(mode, v, a, (hipStream_t)stream);
 }
 
 }  // namespace
@@ -400,6 +454,81 @@ int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
   return sparselnr_spmm(rowptr, colidx, Y, E, A, N, M, L, stream);
 }
 
+int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
+                                    const float *vals, const float *C, const float *D,
+                                    const float *F, const float *Wm, float *A, int64_t N,
+                                    int64_t M, int64_t K, int64_t L, int64_t Mo, void *stream) {
+  if (bad_size(N, M, K, L) || Mo < 0) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!C || !Wm || !A || (M > 0 && (!D || !F)))) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, L > Mo ? L : Mo);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || Mo == 0) return SPARSELNR_OK;
+  if (K != L || !(aligned16(C) && aligned16(D) && aligned16(F) && aligned16(Wm) &&
+                  aligned16(A) && offsets32(M, K) && offsets32(M, L)))
+    return SPARSELNR_ERR_UNSUPPORTED;
+  return run_epilogue(kFused, false, rowptr, colidx, vals, C, D, F, nullptr, Wm, A, N, K, L, Mo,
+                      stream);
+}
+
+int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *colidx, const float *vals,
+                        const float *C, const float *D, float *A, int64_t N, int64_t M,
+                        int64_t K, int64_t L, void *stream) {
+  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && (!A || (K > 0 && !D) || (M > 0 && K > 0 && !C)))
+    return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  if (!(aligned16(C) && aligned16(D) && aligned16(A) && offsets32(M, K)))
+    return SPARSELNR_ERR_UNSUPPORTED;
+  return run_epilogue(kSpmm, false, rowptr, colidx, vals, nullptr, nullptr, C, nullptr, D, A, N,
+                      0, K, L, stream);
+}
+
+int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx, const float *vals,
+                         const float *C, const float *D, const float *E, float *A, int64_t N,
+                         int64_t M, int64_t J, int64_t L, void *stream) {
+  if (bad_size(N, M, J, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && (!A || (J > 0 && !E) || (M > 0 && J > 0 && (!C || !D))))
+    return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, J, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  if (!(aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A) && offsets32(M, J)))
+    return SPARSELNR_ERR_UNSUPPORTED;
+  return run_epilogue(kSpmm, true, rowptr, colidx, vals, nullptr, nullptr, C, D, E, A, N, 0, J,
+                      L, stream);
+}
+
+int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,
+                                  const float *vals, const float *C, const float *Dt,
+                                  const float *E, float *A, int64_t N, int64_t M, int64_t K,
+                                  int64_t L, void *stream) {
+  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && K > 0 && !Dt) return SPARSELNR_ERR_INVALID_ARG;
+  int rc = check_range(N, M, K, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  if (M == 0 || K == 0)  // D is empty: nothing to transpose
+    return sparselnr_fused_sddmm_spmm(rowptr, colidx, vals, C, Dt, E, A, N, M, K, L, stream);
+  int dev = 0;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  void *ws = nullptr;
+  if ((rc = get_workspace(dev, s, (size_t)M * K * sizeof(float), &ws, 1)) != SPARSELNR_OK)
+    return rc;
+  float *D = (float *)ws;
+  const int64_t tiles_c = (M + 31) / 32, tiles_r = (K + 31) / 32;
+  hipLaunchKernelGGL(slnr::transpose_kernel, dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0,
+                     s, Dt, D, K, M, tiles_c);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e);
+  return sparselnr_fused_sddmm_spmm(rowptr, colidx, vals, C, D, E, A, N, M, K, L, stream);
+}
+
 int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx, int64_t N, int64_t M,
                            int64_t colidx_len, int64_t *nnz_out, void *stream) {
   if (N < 0 || M < 0 || colidx_len < 0 || !rowptr) return SPARSELNR_ERR_INVALID_ARG;
@@ -437,7 +566,7 @@ int sparselnr_release(void) {
   (void)hipGetDevice(&saved);
   for (auto &kv : g_workspace) {
     if (!kv.second.ptr) continue;
-    hipError_t e = hipSetDevice(kv.first.first);
+    hipError_t e = hipSetDevice(kv.first.dev);
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e == hipSuccess) e = hipFree(kv.second.ptr);
     if (e != hipSuccess) rc = hip_fail(e);

@@ -74,6 +74,10 @@ struct WalkArgs {
   int32_t min_chunk;  // smallest merge-path slice per worker
   int32_t xcd_span;   // blocks per XCD for the XCD-contiguous remap (0: off)
   int32_t xcds;       // XCDs the hardware deals blocks across
+  // consumer row width and the optional parts of the Section 6.2 benchmarks
+  int32_t Lin;        // width of the gathered consumer rows (E, G2); == L without epilogue
+  const float *G2;    // second gathered row source, multiplied elementwise (M x Lin)
+  const float *Wep;   // per-row epilogue matrix (Lin x L): A_i = t_i * Wep
 };
 
 // ---------------------------------------------------------------- lane ops
@@ -285,10 +289,11 @@ __device__ __forceinline__ Slice make_slice(const WalkArgs &a) {
 }
 
 // Registers holding one nonzero's gathered rows.
-template <int MODE, int KV, int LV>
+template <int MODE, int KV, int LV, int HAD>
 struct Gather {
   float d[MODE == kSpmm ? 1 : KV];
   float e[MODE == kSddmm ? 1 : LV];
+  float h[HAD ? LV : 1];
   float b;
 };
 
@@ -299,6 +304,11 @@ struct Gather {
 // KV  floats of C_i / D_j per producer lane (K = PS * KV).
 // LV  floats of E_j / A_i per lane (L = W * LV).
 // SCHED, U  gather schedule and, for kPaced, the nonzeros per step.
+// HAD  the consumer row is E_j .* G2_j (Hadamard product of two gathers).
+// LVO  0, or the epilogue width per lane: the finished row t_i (W * LV
+//      wide) is multiplied by Wep (staged in LDS) and W * LVO floats are
+//      stored.  The epilogue is linear, so partial rows of split rows take it
+//      too and the carry fixup adds the products.
 //
 // Per worker the state is group-uniform (all W lanes agree on i, p, n), so
 // lane-group divergence inside a wave only masks whole groups.  Three small
@@ -306,9 +316,20 @@ struct Gather {
 // path: rowptr (row ends), colidx and vals.  C_i, the CSR arrays and A are
 // streamed once per call and carry the nontemporal hint; the gathered D_j and
 // E_j rows are plain loads so the hot columns stay in L2.
-template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U>
+template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U, int HAD = 0, int LVO = 0>
 __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
   constexpr int PS = W / NB;
+  static_assert((HAD == 0 && LVO == 0) || (NB == 1 && SCHED == kPipelined && MODE != kSddmm),
+                "Hadamard rows and epilogues use the pipelined one-dot schedule");
+  constexpr int LOUT = LVO ? W * LVO : W * LV;  // width of a stored row
+  extern __shared__ float smem[];
+  if constexpr (LVO > 0) {
+    // stage Wep (Lin x LOUT) once per block, before any worker leaves
+    const int total = W * LV * LOUT;
+    for (int t = threadIdx.x * 4; t < total; t += blockDim.x * 4)
+      *reinterpret_cast<f4_t *>(smem + t) = *reinterpret_cast<const f4_t *>(a.Wep + t);
+    __syncthreads();
+  }
   static_assert(W >= 4 && W <= 64 && (W & (W - 1)) == 0, "W");
   static_assert(NB >= 1 && W % NB == 0, "NB");
   static_assert(SCHED == kPipelined || (U >= 1 && U <= W && (NB == 1 || U == NB)), "U");
@@ -331,7 +352,7 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
   const int64_t K = a.K, L = a.L, N = a.N;
   constexpr int64_t kFar = -((int64_t)1 << 40);
   // byte strides of D and E rows and this lane's byte offset inside a row
-  const uint32_t strideD = (uint32_t)K * 4u, strideE = (uint32_t)L * 4u;
+  const uint32_t strideD = (uint32_t)K * 4u, strideE = (uint32_t)a.Lin * 4u;
   const uint32_t offD = (uint32_t)(q * KV) * 4u, offE = (uint32_t)(glane * LV) * 4u;
 
   int64_t i = s.i0, p = s.p0;
@@ -351,6 +372,7 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
       }
       r_end = bperm_i(gbase + (int)(i + 1 - rb), wr);
     }
+    const int64_t row_start = p;  // first nonzero of this row inside the slice
     float acc[LV];
 #pragma unroll
     for (int v = 0; v < LV; ++v) acc[v] = 0.f;
@@ -420,16 +442,17 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
         // while nonzero u-1 is reduced and applied.  The loop body is
         // straight-line, so the wait before each consume covers exactly the
         // older pair of loads.
-        Gather<MODE, KV, LV> ga, gb;
+        Gather<MODE, KV, LV, HAD> ga, gb;
         float ysel = 0.f;
-        auto issue = [&](Gather<MODE, KV, LV> &g, int u) {
+        auto issue = [&](Gather<MODE, KV, LV, HAD> &g, int u) {
           const int src = gbase + off + u;
           const uint32_t j = (uint32_t)bperm_i(src, wj);
           g.b = bperm_f(src, wv);
           if constexpr (MODE != kSpmm) ldv_off<KV>(g.d, Dm, j * strideD + offD);
           if constexpr (MODE != kSddmm) ldv_off<LV>(g.e, Em, j * strideE + offE);
+          if constexpr (HAD) ldv_off<LV>(g.h, a.G2, j * strideE + offE);
         };
-        auto consume = [&](const Gather<MODE, KV, LV> &g, int u) {
+        auto consume = [&](const Gather<MODE, KV, LV, HAD> &g, int u) {
           float y;
           if constexpr (MODE == kSpmm) {
             y = g.b;
@@ -442,6 +465,9 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
           }
           if constexpr (MODE == kSddmm) {
             if (glane == u) ysel = y;
+          } else if constexpr (HAD) {
+#pragma unroll
+            for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v] * g.h[v], acc[v]);
           } else {
 #pragma unroll
             for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v], acc[v]);
@@ -542,10 +568,33 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
       }
       p += n;
     }
-    if (MODE != kSddmm) {
+    if constexpr (MODE != kSddmm && LVO == 0) {
       if (!has_end) stv<LV>(a.carry + (worker * 2 + 1) * (int64_t)a.Lw + glane * LV, acc);
       else if (i == s.i0 && s.head) stv<LV>(a.carry + (worker * 2) * (int64_t)a.Lw + glane * LV, acc);
       else stv<LV, kNT>(out + i * L + glane * LV, acc);
+    } else if constexpr (LVO > 0) {
+      // epilogue: o = t_i * Wep, t_i broadcast lane by lane with ds_bpermute
+      // (lane q of the worker holds t_i[q*LV .. q*LV+LV-1]), Wep read from LDS
+      float o[LVO];
+#pragma unroll
+      for (int v = 0; v < LVO; ++v) o[v] = 0.f;
+      if (p > row_start) {
+        const float *wcol = smem + glane * LVO;
+#pragma unroll 2
+        for (int qq = 0; qq < W; ++qq) {
+#pragma unroll
+          for (int e = 0; e < LV; ++e) {
+            const float tl = bperm_f(gbase + qq, acc[e]);
+            float w[LVO];
+            ldv<LVO>(w, wcol + (qq * LV + e) * LOUT);
+#pragma unroll
+            for (int v = 0; v < LVO; ++v) o[v] = fmaf(tl, w[v], o[v]);
+          }
+        }
+      }
+      if (!has_end) stv<LVO>(a.carry + (worker * 2 + 1) * (int64_t)a.Lw + glane * LVO, o);
+      else if (i == s.i0 && s.head) stv<LVO>(a.carry + (worker * 2) * (int64_t)a.Lw + glane * LVO, o);
+      else stv<LVO, kNT>(out + i * L + glane * LVO, o);
     }
     if (!has_end) break;
     ++i;
@@ -672,6 +721,30 @@ __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
     }
     sum += carry[(c * 2) * Lw + l];
     A[(int64_t)r * L + l0 + l] = sum;
+  }
+}
+
+// ------------------------------------------------------------ transpose
+//
+// dst (cols x rows) = src (rows x cols) transposed, through a 32 x 32 tile in
+// LDS so that both the reads and the writes are coalesced.  Block 32 x 8.
+__global__ __launch_bounds__(256) void transpose_kernel(const float *__restrict__ src,
+                                                        float *__restrict__ dst, int64_t rows,
+                                                        int64_t cols, int64_t tiles_c) {
+  __shared__ float tile[32][33];
+  const int64_t tr = blockIdx.x / tiles_c, tc = blockIdx.x % tiles_c;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int64_t r0 = tr * 32, c0 = tc * 32;
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    const int64_t r = r0 + ty + k, c = c0 + tx;
+    if (r < rows && c < cols) tile[ty + k][tx] = src[r * cols + c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    const int64_t c = c0 + ty + k, r = r0 + tx;
+    if (r < rows && c < cols) dst[c * rows + r] = tile[tx][ty + k];
   }
 }
 

@@ -1,0 +1,139 @@
+"""GPU parity for the further computations built on the same hot path: the
+<SDDMM, SpMM, GEMM>, <SpMM, GEMM> and <SpMMH, GEMM> benchmarks of the paper's
+Section 6.2 (sparse row product, then a per-row dense product in the same
+pass) and <SDDMM, SpMM> with D stored transposed (Section 4.3.1).  Same rule
+as tests/parity.py: per row, max error <= 1e-4 * the abs-value scale."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2205_11622_amd as slnr
+import synth
+from tests.gpu_util import make_problem, power_law_lengths, sample_rows
+from tests.parity import assert_rows_close
+
+pytestmark = pytest.mark.gpu
+
+
+def dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda:0")
+
+
+def csr(p):
+    return dev(p.rowptr), dev(p.colidx), dev(p.vals)
+
+
+def rows_of(A, rows):
+    import torch
+    if rows is None:
+        return A.cpu().numpy()
+    return A[torch.from_numpy(rows).to(A.device)].cpu().numpy()
+
+
+def lengths(seed):
+    n = power_law_lengths(2501, seed=seed, cap=5000)
+    n[3] = 7000
+    return n
+
+
+@pytest.mark.parametrize("L,Mo", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+def test_sddmm_spmm_gemm(gpu, L, Mo):
+    p = make_problem(lengths(L + Mo), 2000, L, L, seed=L, dense="normal")
+    W = synth.normal(5, 9, (L, Mo))
+    A = slnr.sparselnr_fused_sddmm_spmm_gemm(*csr(p), dev(p.C), dev(p.D), dev(p.E), dev(W))
+    ref, scale, _ = oracle.sddmm_spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, W)
+    assert_rows_close(rows_of(A, None), ref, scale)
+
+
+@pytest.mark.parametrize("K,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+def test_spmm_gemm(gpu, K, L):
+    p = make_problem(lengths(K + 2 * L), 1800, K, K, seed=K + L, dense="normal")
+    C = p.D                               # M x K rows gathered by the SpMM
+    Dk = synth.normal(3, 9, (K, L))       # K x L dense factor
+    A = slnr.sparselnr_spmm_gemm(*csr(p), dev(C), dev(Dk))
+    ref, scale, _ = oracle.spmm_gemm_rows(p.rowptr, p.colidx, p.vals, C, Dk)
+    assert_rows_close(rows_of(A, None), ref, scale)
+
+
+@pytest.mark.parametrize("J,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+def test_spmmh_gemm(gpu, J, L):
+    p = make_problem(lengths(J + 3 * L), 1700, J, J, seed=J * L, dense="normal")
+    C, D = p.D, p.E                       # M x J each
+    E = synth.normal(4, 9, (J, L))
+    A = slnr.sparselnr_spmmh_gemm(*csr(p), dev(C), dev(D), dev(E))
+    ref, scale, _ = oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, C, D, E)
+    assert_rows_close(rows_of(A, None), ref, scale)
+
+
+@pytest.mark.parametrize("K,L", [(32, 32), (128, 128), (16, 256), (3, 5), (64, 64)])
+def test_transposed_D(gpu, K, L):
+    p = make_problem(lengths(K + L), 2200, K, L, seed=K + 7 * L, dense="normal")
+    Dt = np.ascontiguousarray(p.D.T)      # K x M
+    A = slnr.sparselnr_fused_sddmm_spmm_dt(*csr(p), dev(p.C), dev(Dt), dev(p.E))
+    ref, scale, _ = oracle.fused_rows_dt(p.rowptr, p.colidx, p.vals, p.C, Dt, p.E)
+    assert_rows_close(rows_of(A, None), ref, scale)
+    # the same numbers as the plain layout (same kernel after the transpose)
+    A0 = slnr.sparselnr_fused_sddmm_spmm(*csr(p), dev(p.C), dev(p.D), dev(p.E))
+    import torch
+    assert torch.equal(A, A0)
+
+
+def test_next_empty_and_zero_rows(gpu):
+    import torch
+    p = make_problem(np.zeros(700, np.int64), 50, 64, 64)
+    rp, ci, v = csr(p)
+    A = torch.full((p.N, 32), float("nan"), device="cuda:0")
+    slnr.sparselnr_spmm_gemm(rp, ci, v, dev(p.D), dev(synth.normal(1, 1, (64, 32))), A)
+    assert bool((A == 0).all())
+    A = torch.full((p.N, 64), float("nan"), device="cuda:0")
+    slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, dev(p.C), dev(p.D), dev(p.E),
+                                         dev(synth.normal(1, 2, (64, 64))), A)
+    assert bool((A == 0).all())
+
+
+def test_next_deterministic(gpu):
+    import torch
+    p = make_problem(lengths(99), 1500, 128, 128, seed=99)
+    W = dev(synth.normal(2, 2, (128, 128)))
+    args = (*csr(p), dev(p.D), dev(p.E), W)
+    A1 = slnr.sparselnr_spmmh_gemm(*args).clone()
+    A2 = slnr.sparselnr_spmmh_gemm(*args)
+    assert torch.equal(A1.view(torch.int32), A2.view(torch.int32))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("kernel", ["sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt"])
+def test_next_on_rmat1m(gpu, kernel):
+    """The R-MAT 2^20 structure at the inner sizes the paper uses for each
+    benchmark (K=L=M=64; K=128, L=64; J=L=128), sampled rows."""
+    import torch
+    base = synth.config("rmat1m")
+    rows = sample_rows(base, n_random=1500)
+    rp, ci, v = csr(base)
+    if kernel == "sddmm_spmm_gemm":
+        C, D, F = (synth.normal(0, s, (base.N, 64)) for s in (3, 4, 5))
+        W = synth.normal(0, 6, (64, 64))
+        A = slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, dev(C), dev(D), dev(F), dev(W))
+        ref, scale, _ = oracle.sddmm_spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, F,
+                                                    W, rows=rows)
+    elif kernel == "spmm_gemm":
+        C, Dk = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 6, (128, 64))
+        A = slnr.sparselnr_spmm_gemm(rp, ci, v, dev(C), dev(Dk))
+        ref, scale, _ = oracle.spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, Dk,
+                                              rows=rows)
+    elif kernel == "spmmh_gemm":
+        C, D = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 5, (base.N, 128))
+        E = synth.normal(0, 6, (128, 128))
+        A = slnr.sparselnr_spmmh_gemm(rp, ci, v, dev(C), dev(D), dev(E))
+        ref, scale, _ = oracle.spmmh_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, E,
+                                               rows=rows)
+    else:
+        Dt = np.ascontiguousarray(base.D.T)
+        A = slnr.sparselnr_fused_sddmm_spmm_dt(rp, ci, v, dev(base.C), dev(Dt), dev(base.E))
+        ref, scale, _ = oracle.fused_rows_dt(base.rowptr, base.colidx, base.vals, base.C, Dt,
+                                             base.E, rows=rows)
+    assert_rows_close(rows_of(A, rows), ref, scale, what=kernel)
+    assert not bool(torch.isnan(A).any())
+    del A
+    torch.cuda.empty_cache()
