@@ -1,17 +1,28 @@
 #!/usr/bin/env python3
 """Benchmark of the fused SDDMM->SpMM hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config rmat1m]
+    python bench.py [--steps K] [--warmup W] [--config rmat1m] [--kernel sddmm_spmm]
 
-One step is one call of sparselnr_fused_sddmm_spmm over the whole matrix
-(merge-path walk kernel + carry fixup kernel), inputs resident in HBM.  The
-default workload is the R-MAT graph with 2^20 vertices, 16 edges per vertex
-drawn (duplicates merged, 16,085,851 nonzeros), K = L = 128, seed 0.
+One step is one library call over the whole matrix (merge-path walk kernel +
+carry fixup kernel), inputs resident in HBM.  The default is
+sparselnr_fused_sddmm_spmm on the R-MAT graph with 2^20 vertices, 16 edges
+per vertex drawn (duplicates merged, 16,085,851 nonzeros), K = L = 128,
+seed 0.
 
-Prints ONE JSON line with throughput (Gnnz/s), the roofline of the fused
-call against MI355X HBM peak (algorithmic bytes of the fused schedule:
-CSR arrays + one gathered D row and E row per nonzero + C and A streams),
-the in-library unfused comparison, and the CPU oracle timed on the host.
+Prints ONE JSON line with throughput (Gnnz/s), the roofline of the call
+against MI355X HBM peak (algorithmic bytes of the fused schedule: CSR arrays
++ the gathered dense rows per nonzero + the dense row streams), an in-run
+comparison with the same result computed in separate passes, and the CPU
+oracle timed on the host.
+
+--kernel picks one of the further computations of the paper's Section 6.2
+instead, each on the --config sparsity structure at the inner sizes the
+paper uses for it:
+
+  sddmm_spmm_gemm  A = ((B .* C D^T) F) W,  K = L = Mo = 64
+  spmm_gemm        A = (B C) D,             C is M x 128, D is 128 x 64
+  spmmh_gemm       A = (B (C .* D)) E,      C, D are M x 128, E is 128 x 128
+  dt               <SDDMM, SpMM> with D stored transposed (K x M), K = L = 128
 """
 from __future__ import annotations
 
@@ -29,6 +40,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 METRIC = "fused SDDMM→SpMM Gnnz/s + achieved HBM GB/s vs peak, R-MAT 1M rows K=L=128"
 KERNEL_SOURCES = ["paper_2205_11622_amd/csrc/walker.hpp", "paper_2205_11622_amd/csrc/sparselnr.hip"]
+KERNELS = ("sddmm_spmm", "sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt")
+CPU_SECONDS = 10.0  # oracle passes are repeated until about this much wall time
 
 
 def source_digest() -> str:
@@ -39,10 +52,14 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(config: str):
-    """HBM traffic per fused call from committed rocprofv3 counter runs, only
-    if they were taken on the kernel sources as they are now."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % config)
+def workload_key(config: str, kernel: str) -> str:
+    return config if kernel == "sddmm_spmm" else "%s_%s" % (config, kernel)
+
+
+def stored_traffic(key: str):
+    """HBM traffic per call from committed rocprofv3 counter runs, only if they
+    were taken on the kernel sources as they are now."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % key)
     if not os.path.exists(path):
         return None
     with open(path) as fh:
@@ -52,14 +69,157 @@ def stored_traffic(config: str):
     return t
 
 
+def make_workload(kernel, config, dev):
+    """Inputs on the device, the timed call, the comparison call, the byte model
+    and the oracle leg for one kernel."""
+    import numpy as np
+    import torch
+
+    import paper_2205_11622_amd as slnr
+    import synth
+
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    base = synth.config(config)
+    N, M, nnz = base.N, base.M, base.nnz
+    rp, ci, v = t(base.rowptr), t(base.colidx), t(base.vals)
+    w = {"N": N, "M": M, "nnz": nnz, "seed": 0}
+    desc = "%s: %s" % (config, synth.CONFIGS[config]["desc"])
+    csr_bytes = 4 * (N + 1) + 8 * nnz
+
+    if kernel == "sddmm_spmm":
+        p = base
+        C, D, E = t(p.C), t(p.D), t(p.E)
+        A = torch.empty((N, p.L), dtype=torch.float32, device=dev)
+        Y = torch.empty(nnz, dtype=torch.float32, device=dev)
+        A2 = torch.empty_like(A)
+        w.update(K=p.K, L=p.L)
+        return dict(
+            metric=METRIC, desc=desc, sizes=w,
+            call=lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A, stream=stream),
+            compare=lambda: slnr.sparselnr_unfused_sddmm_spmm(rp, ci, v, C, D, E, Y, A2,
+                                                              stream=stream),
+            compare_desc="library unfused path: sparselnr_sddmm into an nnz-sized Y, then "
+                         "sparselnr_spmm",
+            bytes=p.model_bytes(), bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
+            dominant="walk_fast fused + carry_fixup (one call)",
+            oracle=lambda: __import__("oracle").fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D,
+                                                           p.E))
+
+    if kernel == "sddmm_spmm_gemm":
+        K = L = Mo = 64
+        Ch, Dh, Fh = (synth.normal(0, s, (n, K)) for s, n in ((3, N), (4, M), (5, M)))
+        Wh = synth.normal(0, 6, (L, Mo))
+        C, D, F, W = t(Ch), t(Dh), t(Fh), t(Wh)
+        A = torch.empty((N, Mo), dtype=torch.float32, device=dev)
+        T = torch.empty((N, L), dtype=torch.float32, device=dev)
+        A2 = torch.empty_like(A)
+
+        def two_pass():
+            slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, F, T, stream=stream)
+            torch.mm(T, W, out=A2)
+        w.update(K=K, L=L, Mo=Mo)
+        return dict(
+            metric="fused <SDDMM,SpMM,GEMM> Gnnz/s + achieved HBM GB/s vs peak, "
+                   "%s K=L=M=64" % config, desc=desc, sizes=w,
+            call=lambda: slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, C, D, F, W, A,
+                                                              stream=stream),
+            compare=two_pass,
+            compare_desc="sparselnr_fused_sddmm_spmm into an N x L temporary, then torch.mm "
+                         "by W",
+            bytes=csr_bytes + 4 * nnz * (K + L) + 4 * N * K + 4 * N * Mo + 4 * L * Mo,
+            bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N Mo + 4 L Mo",
+            dominant="walk_fast fused with per-row GEMV epilogue + carry_fixup (one call)",
+            oracle=lambda: __import__("oracle").sddmm_spmm_gemm_rows(
+                base.rowptr, base.colidx, base.vals, Ch, Dh, Fh, Wh))
+
+    if kernel == "spmm_gemm":
+        K, L = 128, 64
+        Ch = synth.normal(0, 4, (M, K))
+        Dh = synth.normal(0, 6, (K, L))
+        C, D = t(Ch), t(Dh)
+        A = torch.empty((N, L), dtype=torch.float32, device=dev)
+        T = torch.empty((N, K), dtype=torch.float32, device=dev)
+        A2 = torch.empty_like(A)
+
+        def two_pass():
+            slnr.sparselnr_spmm(rp, ci, v, C, T, stream=stream)
+            torch.mm(T, D, out=A2)
+        w.update(K=K, L=L)
+        return dict(
+            metric="fused <SpMM,GEMM> Gnnz/s + achieved HBM GB/s vs peak, %s K=128 L=64"
+                   % config, desc=desc, sizes=w,
+            call=lambda: slnr.sparselnr_spmm_gemm(rp, ci, v, C, D, A, stream=stream),
+            compare=two_pass,
+            compare_desc="sparselnr_spmm (B C) into an N x K temporary, then torch.mm by D",
+            bytes=csr_bytes + 4 * nnz * K + 4 * K * L + 4 * N * L,
+            bytes_model="4(N+1) + 8 nnz + 4 nnz K + 4 K L + 4 N L",
+            dominant="walk_fast SpMM with per-row GEMV epilogue + carry_fixup (one call)",
+            oracle=lambda: __import__("oracle").spmm_gemm_rows(base.rowptr, base.colidx,
+                                                               base.vals, Ch, Dh))
+
+    if kernel == "spmmh_gemm":
+        J, L = 128, 128
+        Ch, Dh = synth.normal(0, 4, (M, J)), synth.normal(0, 5, (M, J))
+        Eh = synth.normal(0, 6, (J, L))
+        C, D, E = t(Ch), t(Dh), t(Eh)
+        A = torch.empty((N, L), dtype=torch.float32, device=dev)
+        H = torch.empty((M, J), dtype=torch.float32, device=dev)
+        T = torch.empty((N, J), dtype=torch.float32, device=dev)
+        A2 = torch.empty_like(A)
+
+        def two_pass():
+            torch.mul(C, D, out=H)
+            slnr.sparselnr_spmm(rp, ci, v, H, T, stream=stream)
+            torch.mm(T, E, out=A2)
+        w.update(J=J, L=L)
+        return dict(
+            metric="fused <SpMMH,GEMM> Gnnz/s + achieved HBM GB/s vs peak, %s J=L=128" % config,
+            desc=desc, sizes=w,
+            call=lambda: slnr.sparselnr_spmmh_gemm(rp, ci, v, C, D, E, A, stream=stream),
+            compare=two_pass,
+            compare_desc="torch.mul C .* D into an M x J temporary, sparselnr_spmm into an "
+                         "N x J temporary, then torch.mm by E",
+            bytes=csr_bytes + 8 * nnz * J + 4 * J * L + 4 * N * L,
+            bytes_model="4(N+1) + 8 nnz + 8 nnz J + 4 J L + 4 N L",
+            dominant="walk_fast Hadamard SpMM with per-row GEMV epilogue + carry_fixup "
+                     "(one call)",
+            oracle=lambda: __import__("oracle").spmmh_gemm_rows(base.rowptr, base.colidx,
+                                                                base.vals, Ch, Dh, Eh))
+
+    if kernel == "dt":
+        p = base
+        Dth = np.ascontiguousarray(p.D.T)
+        C, D, Dt, E = t(p.C), t(p.D), t(Dth), t(p.E)
+        A = torch.empty((N, p.L), dtype=torch.float32, device=dev)
+        A2 = torch.empty_like(A)
+        w.update(K=p.K, L=p.L)
+        return dict(
+            metric="fused SDDMM→SpMM with D stored K x M, Gnnz/s + achieved HBM GB/s vs peak, "
+                   "%s K=L=%d" % (config, p.K), desc=desc, sizes=w,
+            call=lambda: slnr.sparselnr_fused_sddmm_spmm_dt(rp, ci, v, C, Dt, E, A,
+                                                            stream=stream),
+            compare=lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A2,
+                                                            stream=stream),
+            compare_desc="sparselnr_fused_sddmm_spmm on D stored M x K (the cost of the layout)",
+            bytes=p.model_bytes() + 8 * M * p.K,
+            bytes_model="8 M K (transpose pass) + 4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
+            dominant="transpose_kernel + walk_fast fused + carry_fixup (one call)",
+            oracle=lambda: __import__("oracle").fused_rows_dt(p.rowptr, p.colidx, p.vals, p.C,
+                                                              Dth, p.E))
+    raise ValueError(kernel)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="rmat1m")
+    ap.add_argument("--kernel", default="sddmm_spmm", choices=KERNELS)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true",
+                    help="skip the in-run comparison with the separate-pass computation")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -74,30 +234,21 @@ def main() -> int:
     import numpy as np
     import torch
 
-    import paper_2205_11622_amd as slnr
     import synth
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+    if args.config not in synth.CONFIGS:
+        print("unknown config %r" % args.config, file=sys.stderr)
+        return 2
     dev = torch.device("cuda:0")
     t0 = time.time()
-    p = synth.config(args.config)
-    gen_s = time.time() - t0
-    print("# %s: N=%d nnz=%d K=%d L=%d (generated in %.1fs)" % (args.config, p.N, p.nnz, p.K, p.L,
-                                                                gen_s), file=sys.stderr, flush=True)
-    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
-    rowptr, colidx, vals, C, D, E = (t(x) for x in (p.rowptr, p.colidx, p.vals, p.C, p.D, p.E))
-    A = torch.empty((p.N, p.L), dtype=torch.float32, device=dev)
-    Y = torch.empty(p.nnz, dtype=torch.float32, device=dev)
-    A2 = torch.empty_like(A)
+    wl = make_workload(args.kernel, args.config, dev)
+    print("# %s / %s: %s (inputs made in %.1fs)" % (args.config, args.kernel, wl["sizes"],
+                                                    time.time() - t0),
+          file=sys.stderr, flush=True)
     stream = torch.cuda.current_stream(dev)
-
-    def fused():
-        slnr.sparselnr_fused_sddmm_spmm(rowptr, colidx, vals, C, D, E, A, stream=stream)
-
-    def unfused():
-        slnr.sparselnr_unfused_sddmm_spmm(rowptr, colidx, vals, C, D, E, Y, A2, stream=stream)
 
     def timed(fn, steps, warmup):
         for _ in range(warmup):
@@ -114,20 +265,20 @@ def main() -> int:
         per = np.array([ev[s].elapsed_time(ev[s + 1]) for s in range(steps)])
         return per, ev[0].elapsed_time(ev[steps]), wall
 
-    per, total_ms, wall = timed(fused, args.steps, args.warmup)
+    per, total_ms, wall = timed(wl["call"], args.steps, args.warmup)
     ms = total_ms / args.steps
     print("# fused: %.4f ms/call (median %.4f, min %.4f, max %.4f)"
           % (ms, np.median(per), per.min(), per.max()), file=sys.stderr, flush=True)
     unf = None
     if not args.no_unfused:
-        uper, utotal, _ = timed(unfused, args.steps, args.warmup)
+        uper, utotal, _ = timed(wl["compare"], args.steps, args.warmup)
         # interleave a second fused round so both see the same machine state
-        per2, total2, _ = timed(fused, args.steps, 1)
-        unf = {"ms_per_call": utotal / args.steps, "median_ms": float(np.median(uper)),
-               "fused_ms_rerun": total2 / args.steps,
+        per2, total2, _ = timed(wl["call"], args.steps, 1)
+        unf = {"what": wl["compare_desc"], "ms_per_call": utotal / args.steps,
+               "median_ms": float(np.median(uper)), "fused_ms_rerun": total2 / args.steps,
                "fused_speedup": (utotal / args.steps) / ms}
-        print("# unfused: %.4f ms/call; fused rerun %.4f ms" % (unf["ms_per_call"],
-                                                               unf["fused_ms_rerun"]),
+        print("# comparison: %.4f ms/call; fused rerun %.4f ms" % (unf["ms_per_call"],
+                                                                  unf["fused_ms_rerun"]),
               file=sys.stderr, flush=True)
 
     if args.copy_probe:
@@ -138,37 +289,40 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    nnz = p.nnz
-    model_bytes = p.model_bytes()
+    nnz = wl["sizes"]["nnz"]
+    model_bytes = wl["bytes"]
     gnnz = nnz / (ms * 1e-3) / 1e9
     achieved = model_bytes / (ms * 1e-3) / 1e9
-    traffic = stored_traffic(args.config)
+    key = workload_key(args.config, args.kernel)
+    traffic = stored_traffic(key)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": traffic["bytes_per_call"] if traffic else None,
-                "kernel": "walk_fast fused + carry_fixup (one call)",
-                "bytes_per_call": model_bytes,
-                "bytes_model": "4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L"}
+                "kernel": wl["dominant"], "bytes_per_call": model_bytes,
+                "bytes_model": wl["bytes_model"]}
 
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        rows = np.arange(p.N, dtype=np.int64)
+        times = []
         t1 = time.perf_counter()
-        oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, rows=rows)
-        cs = time.perf_counter() - t1
+        while not times or (time.perf_counter() - t1 < CPU_SECONDS and len(times) < 50):
+            s0 = time.perf_counter()
+            wl["oracle"]()
+            times.append(time.perf_counter() - s0)
+        cs = float(np.median(times))
         cpu = {"value": round(nnz / cs / 1e9, 6), "unit": "Gnnz/s", "cores": oracle.num_threads(),
-               "kind": "oracle", "seconds": round(cs, 3),
-               "sample": "the whole %s workload (%d rows, %d nonzeros), one pass, fp64 "
-                         "accumulation, OpenMP over rows" % (args.config, p.N, nnz)}
+               "kind": "oracle", "seconds": round(cs, 3), "passes": len(times),
+               "sample": "the whole %s workload (%d rows, %d nonzeros) per pass, median of %d "
+                         "passes, fp64 accumulation, OpenMP over rows"
+                         % (key, wl["sizes"]["N"], nnz, len(times))}
 
     out = {
-        "metric": METRIC, "value": round(gnnz, 4), "unit": "Gnnz/s", "n_gpus": 1,
+        "metric": wl["metric"], "value": round(gnnz, 4), "unit": "Gnnz/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "%s: %s" % (args.config, synth.CONFIGS[args.config]["desc"]),
-                   "N": p.N, "M": p.M, "nnz": nnz, "K": p.K, "L": p.L, "seed": 0},
+        "config": dict({"workload": wl["desc"], "kernel": args.kernel}, **wl["sizes"]),
         "roofline": roofline, "cpu_baseline": cpu,
         "achieved_GBps": round(achieved, 1),
         "median_ms": round(float(np.median(per)), 5), "wall_s": round(wall, 3),

@@ -126,17 +126,28 @@ struct Variant {
   KernelFn fn = nullptr;
   int W = 64;          // lanes per worker
   bool generic = true; // generic kernel (l-tiles of 256 columns)
-  size_t lds = 0;      // dynamic LDS bytes per block (epilogue matrix + row slots)
+  size_t lds = 0;      // dynamic LDS bytes per block (the epilogue matrix)
+  int block = kBlock;  // threads per block
 };
 
-template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1,
-          int HAD = 0, int LVO = 0>
+template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1>
 Variant fast() {
   Variant v;
-  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, SCHED, U, HAD, LVO>;
+  v.fn = slnr::walk_fast<MODE, W, NB, KV, LV, SCHED, U>;
   v.W = W;
   v.generic = false;
-  if (LVO > 0) v.lds = sizeof(float) * (size_t)W * LV * W * LVO;  // the epilogue matrix
+  return v;
+}
+
+// Epilogue kernel: W-lane workers, Lin = W * LV, tiles of TR rows per wave.
+template <int MODE, int W, int LV, int HAD, int TR>
+Variant epi() {
+  Variant v;
+  v.fn = slnr::walk_epi<MODE, W, LV, HAD, TR>;
+  v.W = W;
+  v.generic = false;
+  constexpr int TS = W * LV + 4;
+  v.lds = (size_t)(kBlock / 64) * TR * (TS * sizeof(float) + sizeof(uint64_t));
   return v;
 }
 
@@ -205,20 +216,16 @@ Variant pick_spmm(int64_t L, bool al) {
   return generic<kSpmm>();
 }
 
-// Section 6.2 benchmarks with a per-row epilogue (pipelined schedule).  The
-// consumer rows are W * 4 wide; the stored rows W * LVO (LVO = 2 or 4).
-template <int MODE, int W, int HAD>
-Variant pick_epi_lvo(int64_t Lout) {
-  if (Lout == 2 * W) return fast<MODE, W, 1, 4, 4, slnr::kPipelined, 1, HAD, 2>();
-  if (Lout == 4 * W) return fast<MODE, W, 1, 4, 4, slnr::kPipelined, 1, HAD, 4>();
-  return Variant{};
-}
-
+// Section 6.2 benchmarks with a per-row epilogue: Lin in {32, 64, 128} (the
+// walk of the plain SpMM of that width), Lout = Lin / 2 or Lin.  Tiles of 16
+// rows per wave, 12 at Lin = 128, where 16 would let LDS limit occupancy
+// (measured on MI355X, R-MAT 2^20 rows).
 template <int MODE, int HAD>
 Variant pick_epi(int64_t Lin, int64_t Lout) {
-  if (Lin == 32) return pick_epi_lvo<MODE, 8, HAD>(Lout);
-  if (Lin == 64) return pick_epi_lvo<MODE, 16, HAD>(Lout);
-  if (Lin == 128) return pick_epi_lvo<MODE, 32, HAD>(Lout);
+  if (Lout != Lin && 2 * Lout != Lin) return Variant{};
+  if (Lin == 32) return epi<MODE, 8, 4, HAD, 16>();
+  if (Lin == 64) return epi<MODE, 16, 4, HAD, 16>();
+  if (Lin == 128) return epi<MODE, 32, 4, HAD, 12>();
   return Variant{};
 }
 
@@ -229,7 +236,7 @@ struct Grid {
 };
 
 // Resident blocks per CU for `fn` (occupancy query, cached per device).
-int blocks_per_cu(int dev, KernelFn fn, size_t lds, int *out) {
+int blocks_per_cu(int dev, KernelFn fn, int block, size_t lds, int *out) {
   std::lock_guard<std::mutex> lock(g_mu);
   if (g_grid_factor == 0) {
     const char *env = getenv("SPARSELNR_GRID_FACTOR");
@@ -243,7 +250,7 @@ int blocks_per_cu(int dev, KernelFn fn, size_t lds, int *out) {
     return SPARSELNR_OK;
   }
   int nb = 0;
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)fn, kBlock, lds);
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, (const void *)fn, block, lds);
   if (e != hipSuccess) return hip_fail(e);
   if (nb <= 0) nb = 1;
   g_occupancy[key] = nb;
@@ -257,16 +264,16 @@ int blocks_per_cu(int dev, KernelFn fn, size_t lds, int *out) {
 // matrices share their D/E rows in L2) and the dispatcher balances the tail.
 // Small matrices (fewer than 8 rows per resident worker) use one resident
 // grid, because extra blocks would only find empty slices.
-Grid make_grid(int cus, int per_cu, int W, int64_t N) {
+Grid make_grid(int cus, int per_cu, int block, int W, int64_t N) {
   Grid g;
   const int64_t resident_blocks = (int64_t)cus * per_cu;
-  const int64_t resident_workers = resident_blocks * (kBlock / 64) * (64 / W);
+  const int64_t resident_workers = resident_blocks * (block / 64) * (64 / W);
   int factor = g_grid_factor;
   if (factor < 1) factor = N >= 8 * resident_workers ? kGridFactor : 1;
   int blocks = (int)(resident_blocks * factor);
   blocks = ((blocks + kXcds - 1) / kXcds) * kXcds;
   g.blocks = blocks;
-  g.workers = blocks * (kBlock / 64) * (64 / W);
+  g.workers = blocks * (block / 64) * (64 / W);
   g.xcd_span = SLNR_XCD_REMAP ? blocks / kXcds : 0;
   return g;
 }
@@ -277,8 +284,8 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
   if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
   if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
   int per_cu = 1;
-  if ((rc = blocks_per_cu(dev, v.fn, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
-  const Grid g = make_grid(cus, per_cu, v.W, a.N);
+  if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
+  const Grid g = make_grid(cus, per_cu, v.block, v.W, a.N);
   a.workers = g.workers;
   a.min_chunk = kMinChunk;
   a.xcd_span = g.xcd_span;
@@ -300,7 +307,7 @@ int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
   for (int64_t t = 0; t < (mode == kSddmm ? 1 : tiles); ++t) {
     a.l0 = (int32_t)(t * tile_w);
     a.Lw = (int32_t)((a.L - a.l0) < tile_w ? (a.L - a.l0) : tile_w);
-    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(kBlock), v.lds, stream, a);
+    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(v.block), v.lds, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e);
     if (mode != kSddmm) {
