@@ -23,6 +23,11 @@ paper uses for it:
   spmm_gemm        A = (B C) D,             C is M x 128, D is 128 x 64
   spmmh_gemm       A = (B (C .* D)) E,      C, D are M x 128, E is 128 x 128
   dt               <SDDMM, SpMM> with D stored transposed (K x M), K = L = 128
+
+--sweep (with --kernel spmm_gemm) instead prints one JSON line per (K, L) in
+{16, 32, 64, 128, 256, 512}^2: the fused call against the separate passes
+(SpMM into an N x K temporary, then torch.mm), the inner-size study of the
+paper's Section 6.3 (Figure 8) on the --config sparsity structure.
 """
 from __future__ import annotations
 
@@ -95,13 +100,16 @@ def make_workload(kernel, config, dev):
         A2 = torch.empty_like(A)
         w.update(K=p.K, L=p.L)
         return dict(
-            metric=METRIC, desc=desc, sizes=w,
+            metric=METRIC if config == "rmat1m" else
+            "fused SDDMM→SpMM Gnnz/s + achieved HBM GB/s vs peak, %s K=%d L=%d" % (config, p.K, p.L),
+            desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A, stream=stream),
             compare=lambda: slnr.sparselnr_unfused_sddmm_spmm(rp, ci, v, C, D, E, Y, A2,
                                                               stream=stream),
             compare_desc="library unfused path: sparselnr_sddmm into an nnz-sized Y, then "
                          "sparselnr_spmm",
             bytes=p.model_bytes(), bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
+            footprint=csr_bytes + 4 * (N * p.K + M * p.K + M * p.L + N * p.L),
             dominant="walk_fast fused + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D,
                                                            p.E))
@@ -129,6 +137,7 @@ def make_workload(kernel, config, dev):
                          "by W",
             bytes=csr_bytes + 4 * nnz * (K + L) + 4 * N * K + 4 * N * Mo + 4 * L * Mo,
             bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N Mo + 4 L Mo",
+            footprint=csr_bytes + 4 * (N * K + M * K + M * L + L * Mo + N * Mo),
             dominant="walk_fast fused with per-row GEMV epilogue + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").sddmm_spmm_gemm_rows(
                 base.rowptr, base.colidx, base.vals, Ch, Dh, Fh, Wh))
@@ -154,6 +163,7 @@ def make_workload(kernel, config, dev):
             compare_desc="sparselnr_spmm (B C) into an N x K temporary, then torch.mm by D",
             bytes=csr_bytes + 4 * nnz * K + 4 * K * L + 4 * N * L,
             bytes_model="4(N+1) + 8 nnz + 4 nnz K + 4 K L + 4 N L",
+            footprint=csr_bytes + 4 * (M * K + K * L + N * L),
             dominant="walk_fast SpMM with per-row GEMV epilogue + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").spmm_gemm_rows(base.rowptr, base.colidx,
                                                                base.vals, Ch, Dh))
@@ -182,6 +192,7 @@ def make_workload(kernel, config, dev):
                          "N x J temporary, then torch.mm by E",
             bytes=csr_bytes + 8 * nnz * J + 4 * J * L + 4 * N * L,
             bytes_model="4(N+1) + 8 nnz + 8 nnz J + 4 J L + 4 N L",
+            footprint=csr_bytes + 4 * (2 * M * J + J * L + N * L),
             dominant="walk_fast Hadamard SpMM with per-row GEMV epilogue + carry_fixup "
                      "(one call)",
             oracle=lambda: __import__("oracle").spmmh_gemm_rows(base.rowptr, base.colidx,
@@ -204,10 +215,58 @@ def make_workload(kernel, config, dev):
             compare_desc="sparselnr_fused_sddmm_spmm on D stored M x K (the cost of the layout)",
             bytes=p.model_bytes() + 8 * M * p.K,
             bytes_model="8 M K (transpose pass) + 4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
+            footprint=csr_bytes + 4 * (N * p.K + 2 * M * p.K + M * p.L + N * p.L),
             dominant="transpose_kernel + walk_fast fused + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").fused_rows_dt(p.rowptr, p.colidx, p.vals, p.C,
                                                               Dth, p.E))
     raise ValueError(kernel)
+
+
+SWEEP_SIZES = (16, 32, 64, 128, 256, 512)
+
+
+def sweep_spmm_gemm(args, dev, timed) -> None:
+    import numpy as np
+    import torch
+
+    import paper_2205_11622_amd as slnr
+    import synth
+
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    base = synth.config(args.config)
+    N, M, nnz = base.N, base.M, base.nnz
+    rp, ci, v = t(base.rowptr), t(base.colidx), t(base.vals)
+    cmax = synth.normal(0, 4, (M, max(SWEEP_SIZES)))
+    for K in SWEEP_SIZES:
+        C = t(cmax[:, :K])
+        T = torch.empty((N, K), dtype=torch.float32, device=dev)
+        for L in SWEEP_SIZES:
+            D = t(synth.normal(0, 6, (K, L)))
+            A = torch.empty((N, L), dtype=torch.float32, device=dev)
+            A2 = torch.empty_like(A)
+
+            def fused():
+                slnr.sparselnr_spmm_gemm(rp, ci, v, C, D, A, stream=stream)
+
+            def separate():
+                slnr.sparselnr_spmm(rp, ci, v, C, T, stream=stream)
+                torch.mm(T, D, out=A2)
+            _, f_ms, _ = timed(fused, args.steps, args.warmup)
+            _, s_ms, _ = timed(separate, args.steps, args.warmup)
+            f_ms /= args.steps
+            s_ms /= args.steps
+            model = 4 * (N + 1) + 8 * nnz + 4 * nnz * K + 4 * K * L + 4 * N * L
+            gbs = model / (f_ms * 1e-3) / 1e9
+            print(json.dumps({"sweep": "spmm_gemm", "config": args.config, "K": K, "L": L,
+                              "fused_ms": round(f_ms, 5), "separate_ms": round(s_ms, 5),
+                              "speedup": round(s_ms / f_ms, 4), "fused_GBps": round(gbs, 1),
+                              "frac": round(gbs / HBM_PEAK_GBPS, 4),
+                              "bytes_model": "4(N+1) + 8 nnz + 4 nnz K + 4 K L + 4 N L"}),
+                  flush=True)
+            del A, A2, D
+        del C, T
+        torch.cuda.empty_cache()
 
 
 def main() -> int:
@@ -220,6 +279,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the in-run comparison with the separate-pass computation")
+    ap.add_argument("--sweep", action="store_true",
+                    help="with --kernel spmm_gemm: fused vs separate passes over K, L in "
+                         "{16..512} (one JSON line per point)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -243,11 +305,6 @@ def main() -> int:
         print("unknown config %r" % args.config, file=sys.stderr)
         return 2
     dev = torch.device("cuda:0")
-    t0 = time.time()
-    wl = make_workload(args.kernel, args.config, dev)
-    print("# %s / %s: %s (inputs made in %.1fs)" % (args.config, args.kernel, wl["sizes"],
-                                                    time.time() - t0),
-          file=sys.stderr, flush=True)
     stream = torch.cuda.current_stream(dev)
 
     def timed(fn, steps, warmup):
@@ -264,6 +321,19 @@ def main() -> int:
         wall = time.perf_counter() - t_start
         per = np.array([ev[s].elapsed_time(ev[s + 1]) for s in range(steps)])
         return per, ev[0].elapsed_time(ev[steps]), wall
+
+    if args.sweep:
+        if args.kernel != "spmm_gemm":
+            print("--sweep is defined for --kernel spmm_gemm", file=sys.stderr)
+            return 2
+        sweep_spmm_gemm(args, dev, timed)
+        return 0
+
+    t0 = time.time()
+    wl = make_workload(args.kernel, args.config, dev)
+    print("# %s / %s: %s (inputs made in %.1fs)" % (args.config, args.kernel, wl["sizes"],
+                                                    time.time() - t0),
+          file=sys.stderr, flush=True)
 
     per, total_ms, wall = timed(wl["call"], args.steps, args.warmup)
     ms = total_ms / args.steps
@@ -325,7 +395,9 @@ def main() -> int:
         "config": dict({"workload": wl["desc"], "kernel": args.kernel}, **wl["sizes"]),
         "roofline": roofline, "cpu_baseline": cpu,
         "achieved_GBps": round(achieved, 1),
-        "median_ms": round(float(np.median(per)), 5), "wall_s": round(wall, 3),
+        "footprint_bytes": wl["footprint"],
+        "median_ms": round(float(np.median(per)), 5), "min_ms": round(float(per.min()), 5),
+        "p90_ms": round(float(np.percentile(per, 90)), 5), "wall_s": round(wall, 3),
         "unfused": unf, "source_digest": source_digest(),
     }
     print(json.dumps(out), flush=True)

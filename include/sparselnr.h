@@ -127,10 +127,11 @@ SPARSELNR_API int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
  *   A(i,m) = sum_{j,k,l} B(i,j) C(i,k) D(j,k) F(j,l) W(l,m)
  * computed as the fused <SDDMM, SpMM> row t_i (Figure 2d) followed, in the
  * same pass, by the per-row product A_i = t_i W, so neither the nnz-sized
- * SDDMM values nor the N x L matrix t is ever stored.
+ * SDDMM values nor the N x L matrix t is ever stored.  The row products
+ * run on the matrix cores over tiles of finished rows.
  *   C: N x K, D: M x K, F: M x L, W: L x Mo, A: N x Mo (overwritten).
- * Supported: K == L in {32, 64, 128} and Mo in {L/2, L}; 16-byte aligned
- * operands.  Other shapes return SPARSELNR_ERR_UNSUPPORTED.
+ * Supported: K == L in {16, 32, 64, 128, 256, 512}, any Mo; C, D and F
+ * 16-byte aligned.  Other shapes return SPARSELNR_ERR_UNSUPPORTED.
  */
 SPARSELNR_API int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
                                     const float *vals, const float *C,
@@ -145,7 +146,7 @@ SPARSELNR_API int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const i
  * computed per row as the SpMM row t_i = sum_j B(i,j) C(j,:) (a vector
  * temporary of length K, Section 6.3) followed by A_i = t_i D.
  *   C: M x K, D: K x L, A: N x L (overwritten).
- * Supported: K in {32, 64, 128} and L in {K/2, K}; 16-byte aligned operands.
+ * Supported: K in {16, 32, 64, 128, 256, 512}, any L; C 16-byte aligned.
  */
 SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
                         const float *vals, const float *C, const float *D,
@@ -157,7 +158,8 @@ SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *coli
  *   A(i,l) = sum_{k,j} B(i,k) C(k,j) D(k,j) E(j,l)
  * computed per row as t_i = sum_k B(i,k) (C(k,:) .* D(k,:)) (length J)
  * followed by A_i = t_i E.  B is N x M; C, D: M x J; E: J x L; A: N x L.
- * Supported: J in {32, 64, 128} and L in {J/2, J}; 16-byte aligned operands.
+ * Supported: J in {16, 32, 64, 128, 256, 512}, any L; C and D 16-byte
+ * aligned.
  */
 SPARSELNR_API int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx,
                          const float *vals, const float *C, const float *D,

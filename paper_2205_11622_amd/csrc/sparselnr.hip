@@ -183,7 +183,9 @@ constexpr int kPU128 = SLNR_PACED_U128;
 
 // Fast variants exist for the widths of the benchmark workloads: K = L in
 // {32, 64, 128, 256} (one 16-byte slice of C/D and of E/A per lane) and the
-// asymmetric K = 16, L = 256 (4-lane dot products, 16 per producer pass).
+// asymmetric K = 16, L = 256 (4-lane dot products, 16 per producer pass);
+// the SpMM alone also at L = 16 and 512 (the widths of the <SpMM, GEMM>
+// sweep).
 Variant pick_fused(int64_t K, int64_t L, bool al) {
   if (al) {
     if (K == 32 && L == 32) return fast<kFused, 8, 1, 4, 4, kFS, kPU>();
@@ -208,25 +210,32 @@ Variant pick_sddmm(int64_t K, bool al) {
 
 Variant pick_spmm(int64_t L, bool al) {
   if (al) {
+    if (L == 16) return fast<kSpmm, 4, 1, 4, 4, kUS, kPU>();
     if (L == 32) return fast<kSpmm, 8, 1, 4, 4, kUS, kPU>();
     if (L == 64) return fast<kSpmm, 16, 1, 4, 4, kUS, kPU>();
     if (L == 128) return fast<kSpmm, 32, 1, 4, 4, kUS, kPU128>();
     if (L == 256) return fast<kSpmm, 64, 1, 4, 4, kUS, kPU>();
+    if (L == 512) return fast<kSpmm, 64, 1, 4, 8, kUS, kPU>();
   }
   return generic<kSpmm>();
 }
 
-// Section 6.2 benchmarks with a per-row epilogue: Lin in {32, 64, 128} (the
-// walk of the plain SpMM of that width), Lout = Lin / 2 or Lin.  Tiles of 16
-// rows per wave, 12 at Lin = 128, where 16 would let LDS limit occupancy
+// Section 6.2 benchmarks with a per-row epilogue.  Lin (the width of the
+// gathered rows and of t_i) in {16, 32, 64, 128, 256, 512}, walked like the
+// plain SpMM of that width; any Lout.  Tiles of 16 rows per wave up to
+// Lin = 64, 12 at 128 and 4 above, so that LDS does not limit occupancy
 // (measured on MI355X, R-MAT 2^20 rows).
 template <int MODE, int HAD>
-Variant pick_epi(int64_t Lin, int64_t Lout) {
-  if (Lout != Lin && 2 * Lout != Lin) return Variant{};
-  if (Lin == 32) return epi<MODE, 8, 4, HAD, 16>();
-  if (Lin == 64) return epi<MODE, 16, 4, HAD, 16>();
-  if (Lin == 128) return epi<MODE, 32, 4, HAD, 12>();
-  return Variant{};
+Variant pick_epi(int64_t Lin) {
+  switch (Lin) {
+    case 16: return epi<MODE, 4, 4, HAD, 16>();
+    case 32: return epi<MODE, 8, 4, HAD, 16>();
+    case 64: return epi<MODE, 16, 4, HAD, 16>();
+    case 128: return epi<MODE, 32, 4, HAD, 12>();
+    case 256: return epi<MODE, 64, 4, HAD, 4>();
+    case 512: return epi<MODE, 64, 8, HAD, 4>();
+    default: return Variant{};
+  }
 }
 
 struct Grid {
@@ -352,8 +361,8 @@ int run_epilogue(Mode mode, bool had, const int32_t *rowptr, const int32_t *coli
                  const float *vals, const float *C, const float *D, const float *E,
                  const float *G2, const float *Wm, float *A, int64_t N, int64_t Kdot,
                  int64_t Lin, int64_t Lout, void *stream) {
-  Variant v = mode == kFused ? pick_epi<kFused, 0>(Lin, Lout)
-                             : (had ? pick_epi<kSpmm, 1>(Lin, Lout) : pick_epi<kSpmm, 0>(Lin, Lout));
+  Variant v = mode == kFused ? pick_epi<kFused, 0>(Lin)
+                             : (had ? pick_epi<kSpmm, 1>(Lin) : pick_epi<kSpmm, 0>(Lin));
   if (!v.fn) return SPARSELNR_ERR_UNSUPPORTED;
   WalkArgs a = base_args(rowptr, colidx, vals, N, Kdot, Lout);
   a.C = C;
@@ -471,8 +480,8 @@ int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const int32_t *colidx
   int rc = check_range(N, M, K, L > Mo ? L : Mo);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || Mo == 0) return SPARSELNR_OK;
-  if (K != L || !(aligned16(C) && aligned16(D) && aligned16(F) && aligned16(Wm) &&
-                  aligned16(A) && offsets32(M, K) && offsets32(M, L)))
+  if (K != L || !(aligned16(C) && aligned16(D) && aligned16(F) && offsets32(M, K) &&
+                  offsets32(M, L)))
     return SPARSELNR_ERR_UNSUPPORTED;
   return run_epilogue(kFused, false, rowptr, colidx, vals, C, D, F, nullptr, Wm, A, N, K, L, Mo,
                       stream);
@@ -488,8 +497,7 @@ int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *colidx, const floa
   int rc = check_range(N, M, K, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
-  if (!(aligned16(C) && aligned16(D) && aligned16(A) && offsets32(M, K)))
-    return SPARSELNR_ERR_UNSUPPORTED;
+  if (!(aligned16(C) && offsets32(M, K))) return SPARSELNR_ERR_UNSUPPORTED;
   return run_epilogue(kSpmm, false, rowptr, colidx, vals, nullptr, nullptr, C, nullptr, D, A, N,
                       0, K, L, stream);
 }
@@ -504,8 +512,7 @@ int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx, const flo
   int rc = check_range(N, M, J, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
-  if (!(aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A) && offsets32(M, J)))
-    return SPARSELNR_ERR_UNSUPPORTED;
+  if (!(aligned16(C) && aligned16(D) && offsets32(M, J))) return SPARSELNR_ERR_UNSUPPORTED;
   return run_epilogue(kSpmm, true, rowptr, colidx, vals, nullptr, nullptr, C, D, E, A, N, 0, J,
                       L, stream);
 }
@@ -528,9 +535,15 @@ int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,
   if ((rc = get_workspace(dev, s, (size_t)M * K * sizeof(float), &ws, 1)) != SPARSELNR_OK)
     return rc;
   float *D = (float *)ws;
-  const int64_t tiles_c = (M + 31) / 32, tiles_r = (K + 31) / 32;
-  hipLaunchKernelGGL(slnr::transpose_kernel, dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0,
-                     s, Dt, D, K, M, tiles_c);
+  if (M % 4 == 0 && K % 4 == 0 && aligned16(Dt)) {
+    const int64_t tiles_c = (M + 63) / 64, tiles_r = (K + 63) / 64;
+    hipLaunchKernelGGL(slnr::transpose4_kernel, dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0,
+                       s, Dt, D, K, M, tiles_c);
+  } else {
+    const int64_t tiles_c = (M + 31) / 32, tiles_r = (K + 31) / 32;
+    hipLaunchKernelGGL(slnr::transpose_kernel, dim3((unsigned)(tiles_r * tiles_c)), dim3(256), 0,
+                       s, Dt, D, K, M, tiles_c);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e);
   return sparselnr_fused_sddmm_spmm(rowptr, colidx, vals, C, D, E, A, N, M, K, L, stream);

@@ -125,14 +125,14 @@ def test_product_package_does_not_touch_the_oracle():
 
 def test_next_entry_points_argument_errors():
     L = slnr.lib()
-    # <SDDMM, SpMM, GEMM>: negative size, NULL W, unsupported shape (K != L)
+    # <SDDMM, SpMM, GEMM>: negative size, NULL W, unsupported shapes (K != L, K = L = 48)
     assert L.sparselnr_fused_sddmm_spmm_gemm(*(FAKE,) * 8, 4, 4, 4, 4, -1, NULL) == \
         slnr.ERR_INVALID_ARG
     assert L.sparselnr_fused_sddmm_spmm_gemm(*(FAKE,) * 6, NULL, FAKE, 4, 4, 4, 4, 4, NULL) == \
         slnr.ERR_INVALID_ARG
     assert L.sparselnr_fused_sddmm_spmm_gemm(*(FAKE,) * 8, 4, 4, 64, 32, 32, NULL) == \
         slnr.ERR_UNSUPPORTED
-    assert L.sparselnr_fused_sddmm_spmm_gemm(*(FAKE,) * 8, 4, 4, 64, 64, 48, NULL) == \
+    assert L.sparselnr_fused_sddmm_spmm_gemm(*(FAKE,) * 8, 4, 4, 48, 48, 48, NULL) == \
         slnr.ERR_UNSUPPORTED
     assert L.sparselnr_fused_sddmm_spmm_gemm(*(NULL,) * 8, 0, 0, 0, 0, 0, NULL) == slnr.OK
     # <SpMM, GEMM>
@@ -143,7 +143,7 @@ def test_next_entry_points_argument_errors():
     # <SpMMH, GEMM>
     assert L.sparselnr_spmmh_gemm(FAKE, FAKE, FAKE, FAKE, NULL, FAKE, FAKE, 4, 4, 4, 4, NULL) == \
         slnr.ERR_INVALID_ARG
-    assert L.sparselnr_spmmh_gemm(*(FAKE,) * 7, 4, 4, 64, 100, NULL) == slnr.ERR_UNSUPPORTED
+    assert L.sparselnr_spmmh_gemm(*(FAKE,) * 7, 4, 4, 100, 64, NULL) == slnr.ERR_UNSUPPORTED
     # transposed D
     assert L.sparselnr_fused_sddmm_spmm_dt(*(FAKE,) * 4, NULL, FAKE, FAKE, 4, 4, 4, 4, NULL) == \
         slnr.ERR_INVALID_ARG

@@ -37,7 +37,8 @@ def lengths(seed):
     return n
 
 
-@pytest.mark.parametrize("L,Mo", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+@pytest.mark.parametrize("L,Mo", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64),
+                                  (16, 48), (256, 100), (512, 64), (64, 1)])
 def test_sddmm_spmm_gemm(gpu, L, Mo):
     p = make_problem(lengths(L + Mo), 2000, L, L, seed=L, dense="normal")
     W = synth.normal(5, 9, (L, Mo))
@@ -46,7 +47,8 @@ def test_sddmm_spmm_gemm(gpu, L, Mo):
     assert_rows_close(rows_of(A, None), ref, scale)
 
 
-@pytest.mark.parametrize("K,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+@pytest.mark.parametrize("K,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64),
+                                 (16, 16), (256, 512), (512, 7), (128, 200)])
 def test_spmm_gemm(gpu, K, L):
     p = make_problem(lengths(K + 2 * L), 1800, K, K, seed=K + L, dense="normal")
     C = p.D                               # M x K rows gathered by the SpMM
@@ -56,7 +58,8 @@ def test_spmm_gemm(gpu, K, L):
     assert_rows_close(rows_of(A, None), ref, scale)
 
 
-@pytest.mark.parametrize("J,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64)])
+@pytest.mark.parametrize("J,L", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64),
+                                 (16, 3), (256, 256), (512, 128)])
 def test_spmmh_gemm(gpu, J, L):
     p = make_problem(lengths(J + 3 * L), 1700, J, J, seed=J * L, dense="normal")
     C, D = p.D, p.E                       # M x J each

@@ -20,9 +20,10 @@ pytestmark = pytest.mark.gpu
 # ---------------------------------------------------------------- variants
 
 # (K, L): the first five have hand-tuned fast variants, the rest go through
-# the generic kernel (odd widths, K != L, tiny widths, wide L needing tiles).
+# the generic kernel (odd widths, K != L, tiny widths, wide L needing tiles);
+# the unfused SpMM also has fast variants at L = 16 and 512.
 WIDTHS = [(32, 32), (64, 64), (128, 128), (256, 256), (16, 256),
-          (1, 1), (3, 5), (16, 16), (20, 36), (17, 300), (64, 520), (128, 64)]
+          (1, 1), (3, 5), (16, 16), (20, 36), (17, 300), (64, 520), (128, 64), (64, 512)]
 
 
 @pytest.mark.parametrize("K,L", WIDTHS)
