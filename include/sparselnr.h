@@ -44,9 +44,11 @@
  *     C must be non-NULL when N > 0 and K > 0; D when N, M, K > 0; E when
  *     N, M, L > 0; A when N > 0 and L > 0; Y (unfused/SDDMM) when N > 0.
  *   - Argument errors are reported BEFORE any HIP call, with no side effect.
- *   - The fused, unfused and SpMM calls use a workspace of a few MB per
- *     (device, stream) for rows whose nonzeros are split between workers; it
- *     is allocated on first use, reused, and freed by sparselnr_release().
+ *   - The fused, unfused and SpMM calls use a workspace per (device, stream)
+ *     for rows whose nonzeros are split between workers (2 partial rows per
+ *     worker: tens of MB for matrices of millions of rows); it is allocated
+ *     on first use, grown when a call needs more, reused, and freed by
+ *     sparselnr_release().
  *     Calls on different streams use different workspaces; calls on one
  *     stream are ordered by the stream.
  *   - Results are deterministic: the same inputs give bit-identical outputs
