@@ -44,7 +44,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, published
 METRIC = "fused SDDMM→SpMM Gnnz/s + achieved HBM GB/s vs peak, R-MAT 1M rows K=L=128"
-KERNEL_SOURCES = ["paper_2205_11622_amd/csrc/walker.hpp", "paper_2205_11622_amd/csrc/sparselnr.hip"]
+KERNEL_SOURCES = ["paper_2205_11622_amd/csrc/walker.hpp", "paper_2205_11622_amd/csrc/epilogue.hpp",
+                  "paper_2205_11622_amd/csrc/sparselnr.hip"]
 KERNELS = ("sddmm_spmm", "sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt")
 CPU_SECONDS = 10.0  # oracle passes are repeated until about this much wall time
 

@@ -11,6 +11,7 @@
 
 #include "sparselnr.h"
 #include "walker.hpp"
+#include "epilogue.hpp"
 
 namespace {
 
