@@ -352,6 +352,15 @@ def main() -> int:
                                                                   unf["fused_ms_rerun"]),
               file=sys.stderr, flush=True)
 
+    # context for comparing runs across machines: the rate of torch's own
+    # 1 GiB device-to-device copy (read + write = 2 GiB moved)
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    _, copy_ms, _ = timed(lambda: dst.copy_(src), 5, 2)
+    copy_gbps = 2 * (1 << 30) / (copy_ms / 5 * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+
     if args.copy_probe:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -370,7 +379,8 @@ def main() -> int:
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": traffic["bytes_per_call"] if traffic else None,
                 "kernel": wl["dominant"], "bytes_per_call": model_bytes,
-                "bytes_model": wl["bytes_model"]}
+                "bytes_model": wl["bytes_model"],
+                "torch_copy_GBps": round(copy_gbps, 1)}
 
     cpu = None
     if not args.no_cpu_baseline:
