@@ -96,10 +96,10 @@ SPARSELNR_API int sparselnr_abi_version(void);
  * nonzero order.  Needs the per-(device, stream) workspace.
  */
 SPARSELNR_API int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
-                               const float *vals, const float *C,
-                               const float *D, const float *E, float *A,
-                               int64_t N, int64_t M, int64_t K, int64_t L,
-                               void *stream);
+                                             const float *vals, const float *C,
+                                             const float *D, const float *E, float *A,
+                                             int64_t N, int64_t M, int64_t K, int64_t L,
+                                             void *stream);
 
 /*
  * Unfused comparison (Figure 2a then Figure 2b, Section 3.1.2): the SDDMM
@@ -107,21 +107,21 @@ SPARSELNR_API int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_
  * reads it.  Same result as the fused call up to rounding order.
  */
 SPARSELNR_API int sparselnr_unfused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
-                                 const float *vals, const float *C,
-                                 const float *D, const float *E, float *Y,
-                                 float *A, int64_t N, int64_t M, int64_t K,
-                                 int64_t L, void *stream);
+                                               const float *vals, const float *C,
+                                               const float *D, const float *E, float *Y,
+                                               float *A, int64_t N, int64_t M, int64_t K,
+                                               int64_t L, void *stream);
 
 /* SDDMM alone (Figure 2a): Y[p] = vals[p] * dot(C(i,:), D(colidx[p],:)). */
 SPARSELNR_API int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx,
-                    const float *vals, const float *C, const float *D,
-                    float *Y, int64_t N, int64_t M, int64_t K, void *stream);
+                                  const float *vals, const float *C, const float *D,
+                                  float *Y, int64_t N, int64_t M, int64_t K, void *stream);
 
 /* SpMM alone (Figure 2b): A(i,:) = sum_{p in row i} Y[p] * E(colidx[p],:).
  * A is overwritten.  Needs the per-(device, stream) workspace. */
 SPARSELNR_API int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
-                   const float *Y, const float *E, float *A, int64_t N,
-                   int64_t M, int64_t L, void *stream);
+                                 const float *Y, const float *E, float *A, int64_t N,
+                                 int64_t M, int64_t L, void *stream);
 
 /*
  * <SDDMM, SpMM, GEMM> (Section 6.2; the recursive application of the fusion
@@ -136,11 +136,11 @@ SPARSELNR_API int sparselnr_spmm(const int32_t *rowptr, const int32_t *colidx,
  * 16-byte aligned.  Other shapes return SPARSELNR_ERR_UNSUPPORTED.
  */
 SPARSELNR_API int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
-                                    const float *vals, const float *C,
-                                    const float *D, const float *F,
-                                    const float *W, float *A, int64_t N,
-                                    int64_t M, int64_t K, int64_t L, int64_t Mo,
-                                    void *stream);
+                                                  const float *vals, const float *C,
+                                                  const float *D, const float *F,
+                                                  const float *W, float *A, int64_t N,
+                                                  int64_t M, int64_t K, int64_t L, int64_t Mo,
+                                                  void *stream);
 
 /*
  * <SpMM, GEMM> (Section 6.2; the GNN hidden-state update):
@@ -151,9 +151,9 @@ SPARSELNR_API int sparselnr_fused_sddmm_spmm_gemm(const int32_t *rowptr, const i
  * Supported: K in {16, 32, 64, 128, 256, 512}, any L; C 16-byte aligned.
  */
 SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *colidx,
-                        const float *vals, const float *C, const float *D,
-                        float *A, int64_t N, int64_t M, int64_t K, int64_t L,
-                        void *stream);
+                                      const float *vals, const float *C, const float *D,
+                                      float *A, int64_t N, int64_t M, int64_t K, int64_t L,
+                                      void *stream);
 
 /*
  * <SpMMH, GEMM> (Section 6.2):
@@ -164,9 +164,9 @@ SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *coli
  * aligned.
  */
 SPARSELNR_API int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx,
-                         const float *vals, const float *C, const float *D,
-                         const float *E, float *A, int64_t N, int64_t M,
-                         int64_t J, int64_t L, void *stream);
+                                       const float *vals, const float *C, const float *D,
+                                       const float *E, float *A, int64_t N, int64_t M,
+                                       int64_t J, int64_t L, void *stream);
 
 /*
  * <SDDMM, SpMM> with D stored transposed (Section 4.3.1: the layout whose
@@ -178,10 +178,10 @@ SPARSELNR_API int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *col
  * sparselnr_fused_sddmm_spmm; the workspace is freed by sparselnr_release().
  */
 SPARSELNR_API int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,
-                                  const float *vals, const float *C,
-                                  const float *Dt, const float *E, float *A,
-                                  int64_t N, int64_t M, int64_t K, int64_t L,
-                                  void *stream);
+                                                const float *vals, const float *C,
+                                                const float *Dt, const float *E, float *A,
+                                                int64_t N, int64_t M, int64_t K, int64_t L,
+                                                void *stream);
 
 /*
  * Checks the CSR preconditions on the device: rowptr[0] == 0, rowptr
@@ -193,8 +193,8 @@ SPARSELNR_API int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int
  * Returns SPARSELNR_OK or SPARSELNR_ERR_INVALID_CSR (or an error code).
  */
 SPARSELNR_API int sparselnr_validate_csr(const int32_t *rowptr, const int32_t *colidx,
-                           int64_t N, int64_t M, int64_t colidx_len,
-                           int64_t *nnz_out, void *stream);
+                                         int64_t N, int64_t M, int64_t colidx_len,
+                                         int64_t *nnz_out, void *stream);
 
 /* Static text for a status code (never NULL). */
 SPARSELNR_API const char *sparselnr_status_string(int status);
