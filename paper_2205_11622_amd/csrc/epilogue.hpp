@@ -17,9 +17,9 @@ namespace slnr {
 // is linear, so the partial rows of a row split between slices take it too
 // and the carry fixup adds them.
 //
-// The walk is the pipelined one of walk_fast (W lanes per worker, LV floats
-// of the row per lane), run as a loop that is uniform across the wave: a
-// worker whose slice is done idles.  A worker that finishes a row with
+// The walk is RowWalk (W lanes per worker, LV floats of the row per lane;
+// the schedule is a template choice), run as a loop that is uniform across
+// the wave: a worker whose slice is done idles.  A worker that finishes a row with
 // nonzeros in its slice writes t_i to its wave's tile in LDS (TR rows, filled
 // in order across the wave's workers) and the row's destination (an A row or
 // a carry slot) beside it.  Once the next round of rows might not fit, the
@@ -29,7 +29,7 @@ namespace slnr {
 // stored by 64 lanes in one coalesced pass per 64 columns.  Wep is read
 // through the caches (it is small and every wave reads it), which leaves LDS
 // to the tiles.
-template <int MODE, int W, int LV, int HAD, int TR>
+template <int MODE, int W, int LV, int HAD, int TR, int SCHED, int U>
 __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
   constexpr int KV = LV;  // fused form: K = Lin
   constexpr int LIN = W * LV;
@@ -48,20 +48,14 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
 
   const Slice s = make_slice<W>(a);
   const int64_t worker = s.id;
+  RowWalk<MODE, W, 1, KV, LV, SCHED, U, HAD> rw(a, s.p1, (uint32_t)LIN * 4u);
   const int32_t *__restrict__ rowptr = a.rowptr;
-  const int32_t *__restrict__ colidx = a.colidx;
-  const float *__restrict__ vals = a.vals;
   const float *__restrict__ Cm = a.C;
-  const float *__restrict__ Dm = a.D;
-  const float *__restrict__ Em = a.E;
-  const float *__restrict__ Gm = a.G2;
   const float *__restrict__ Wm = a.Wep;
   float *__restrict__ out = a.out;
   const int64_t K = a.K, L = a.L, N = a.N;
   const int lout = a.L;
   constexpr int64_t kFar = -((int64_t)1 << 40);
-  const uint32_t strideD = (uint32_t)K * 4u, strideE = (uint32_t)LIN * 4u;
-  const uint32_t offD = (uint32_t)(glane * KV) * 4u, offE = (uint32_t)(glane * LV) * 4u;
 
   // Tile product and stores of rows 0..cnt-1.  All lanes of the wave take
   // part (the caller is in uniform control flow).  Inputs go in blocks of
@@ -128,9 +122,6 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
   int64_t i = s.i0, p = s.p0;
   int64_t rb = kFar;  // rowptr window: wr = rowptr[rb + glane]
   int wr = 0;
-  int64_t wb = kFar;  // nonzero window: wj = colidx[wb + glane], wv = vals[wb + glane]
-  int wj = 0;
-  float wv = 0.f;
   int cnt = 0;  // rows waiting in the tile (the same in every lane)
   bool live = s.active;
   while (__ballot(live) != 0) {
@@ -157,60 +148,7 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
 #pragma unroll
         for (int v = 0; v < KV; ++v) c[v] = 0.f;
         if (MODE == kFused && p < r_end) ldv<KV, kNT>(c, Cm + i * K + glane * KV);
-        while (p < r_end) {
-          if (p >= wb + W) {
-            wb = p;
-            const int64_t pw = wb + glane;
-            if (pw < s.p1) {
-              wj = ld_stream(colidx + pw);
-              wv = ld_stream(vals + pw);
-            }
-          }
-          const int n = (int)(r_end - p < wb + W - p ? r_end - p : wb + W - p);
-          const int off = (int)(p - wb);
-          // depth-2 pipeline, as in walk_fast
-          Gather<MODE, KV, LV, HAD> ga, gb;
-          auto issue = [&](Gather<MODE, KV, LV, HAD> &g, int u) {
-            const int src = gbase + off + u;
-            const uint32_t j = (uint32_t)bperm_i(src, wj);
-            g.b = bperm_f(src, wv);
-            if constexpr (MODE == kFused) ldv_off<KV>(g.d, Dm, j * strideD + offD);
-            ldv_off<LV>(g.e, Em, j * strideE + offE);
-            if constexpr (HAD) ldv_off<LV>(g.h, Gm, j * strideE + offE);
-          };
-          auto consume = [&](const Gather<MODE, KV, LV, HAD> &g) {
-            float y = g.b;
-            if constexpr (MODE == kFused) {
-              float t = 0.f;
-#pragma unroll
-              for (int v = 0; v < KV; ++v) t = fmaf(c[v], g.d[v], t);
-              y *= group_sum<W>(t);
-            }
-            if constexpr (HAD) {
-#pragma unroll
-              for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v] * g.h[v], acc[v]);
-            } else {
-#pragma unroll
-              for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v], acc[v]);
-            }
-          };
-          issue(ga, 0);
-          int u = 1;
-          for (; u + 1 < n; u += 2) {
-            issue(gb, u);
-            consume(ga);
-            issue(ga, u + 1);
-            consume(gb);
-          }
-          if (u < n) {
-            issue(gb, u);
-            consume(ga);
-            consume(gb);
-          } else {
-            consume(ga);
-          }
-          p += n;
-        }
+        rw.row(p, r_end, c, acc);
         // destination: a row of A, or a carry slot of a row split between slices
         int64_t off = i * L;
         bool carry = false;

@@ -297,54 +297,279 @@ struct Gather {
   float b;
 };
 
-// ------------------------------------------------------ fast-path kernel
+// ------------------------------------------------------------ row walk
 //
+// The nonzero loop of one row inside one slice, shared by the walk kernels.
 // W   lanes per worker (4..64); the consumer spreads E_j / A_i over them.
 // NB  nonzeros per producer pass; PS = W / NB lanes form one dot product.
 // KV  floats of C_i / D_j per producer lane (K = PS * KV).
 // LV  floats of E_j / A_i per lane (L = W * LV).
 // SCHED, U  gather schedule and, for kPaced, the nonzeros per step.
+// HAD  the consumer row is E_j .* G2_j (Hadamard product of two gathers).
 //
-// Per worker the state is group-uniform (all W lanes agree on i, p, n), so
-// lane-group divergence inside a wave only masks whole groups.  Three small
-// windows, one entry per lane, keep the dependent loads off the critical
-// path: rowptr (row ends), colidx and vals.  C_i, the CSR arrays and A are
-// streamed once per call and carry the nontemporal hint; the gathered D_j and
-// E_j rows are plain loads so the hot columns stay in L2.
-template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U>
-__global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
-  constexpr int PS = W / NB;
+// The state is group-uniform (all W lanes agree on p, n), so lane-group
+// divergence inside a wave only masks whole groups.  The colidx / vals window
+// (one entry per lane) keeps the dependent loads off the critical path; the
+// gathered D_j and E_j rows are plain loads so the hot columns stay in L2.
+template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U, int HAD = 0>
+struct RowWalk {
+  static constexpr int PS = W / NB;
   static_assert(W >= 4 && W <= 64 && (W & (W - 1)) == 0, "W");
   static_assert(NB >= 1 && W % NB == 0, "NB");
   static_assert(SCHED == kPipelined || (U >= 1 && U <= W && (NB == 1 || U == NB)), "U");
-  const int lane = threadIdx.x & 63;
-  const int glane = lane & (W - 1);
-  const int gbase = lane - glane;
-  const int q = glane % PS;   // k-slice of this lane in its dot product
-  const int sub = glane / PS; // which nonzero of a producer pass (NB > 1)
+  static_assert(!HAD || (NB == 1 && MODE == kSpmm), "Hadamard rows come with the one-dot SpMM");
+
+  const int32_t *__restrict__ colidx;
+  const float *__restrict__ vals;
+  const float *__restrict__ Dm;
+  const float *__restrict__ Em;
+  const float *__restrict__ Gm;
+  float *__restrict__ out;  // SDDMM values (kSddmm)
+  int64_t p1;               // end of the slice's nonzeros
+  uint32_t strideD, strideE, offD, offE;  // row strides and this lane's offset, in bytes
+  int glane, gbase, q, sub;
+  int64_t wb;  // nonzero window: wj = colidx[wb + glane], wv = vals[wb + glane]
+  int wj;
+  float wv;
+
+  __device__ __forceinline__ RowWalk(const WalkArgs &a, int64_t p1_, uint32_t strideE_)
+      : colidx(a.colidx), vals(a.vals), Dm(a.D), Em(a.E), Gm(a.G2), out(a.out), p1(p1_),
+        strideD((uint32_t)a.K * 4u), strideE(strideE_), wb(-((int64_t)1 << 40)), wj(0),
+        wv(0.f) {
+    const int lane = threadIdx.x & 63;
+    glane = lane & (W - 1);
+    gbase = lane - glane;
+    q = glane % PS;    // k-slice of this lane in its dot product
+    sub = glane / PS;  // which nonzero of a producer pass (NB > 1)
+    offD = (uint32_t)(q * KV) * 4u;
+    offE = (uint32_t)(glane * LV) * 4u;
+  }
+
+  // Nonzeros p .. r_end-1 of the current row: their products with C_i (held
+  // in c) are formed and applied to acc (or written out for the SDDMM).
+  __device__ __forceinline__ void row(int64_t &p, int64_t r_end, const float (&c)[KV],
+                                      float (&acc)[LV]) {
+      while (p < r_end) {
+        if (p >= wb + W) {  // refill the nonzero window
+          wb = p;
+          const int64_t pw = wb + glane;
+          if (pw < p1) {
+            wj = kNT ? ld_stream(colidx + pw) : colidx[pw];
+            wv = kNT ? ld_stream(vals + pw) : vals[pw];
+          }
+        }
+        // this step: the row's nonzeros inside the window (at most NB for a
+        // producer pass of the multi-dot variant)
+        int n = (int)(r_end - p < wb + W - p ? r_end - p : wb + W - p);
+        if (NB > 1 && n > NB) n = NB;
+        if (SCHED == kPaced && n > U) n = U;
+        const int off = (int)(p - wb);
+        if constexpr (NB == 1 && SCHED == kPaced) {
+          uint32_t jj[U];
+          float bb[U];
+  #pragma unroll
+          for (int u = 0; u < U; ++u) {  // lanes past n read stale entries, unused
+            const int src = (gbase + off + u) & 63;
+            jj[u] = (uint32_t)bperm_i(src, wj);
+            bb[u] = bperm_f(src, wv);
+          }
+          float dr[U][KV];
+          float er[U][LV];
+          float hr[HAD ? U : 1][HAD ? LV : 1];
+  #pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (u < n) {
+              if (u > 0) wait_vmcnt<1>();
+              if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
+              if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
+              if constexpr (HAD) ldv_off<LV>(hr[u], Gm, jj[u] * strideE + offE);
+            }
+          }
+          float ysel = 0.f;
+  #pragma unroll
+          for (int u = 0; u < U; ++u) {
+            if (u < n) {
+              float y;
+              if constexpr (MODE == kSpmm) {
+                y = bb[u];
+              } else {
+                float t = 0.f;
+  #pragma unroll
+                for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[u][v], t);
+                t = group_sum<W>(t);
+                y = bb[u] * t;
+              }
+              if constexpr (MODE == kSddmm) {
+                if (glane == u) ysel = y;
+              } else if constexpr (HAD) {
+  #pragma unroll
+                for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, er[u][v] * hr[u][v], acc[v]);
+              } else {
+  #pragma unroll
+                for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, er[u][v], acc[v]);
+              }
+            }
+          }
+          if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
+        } else if constexpr (NB == 1) {
+          // Depth-2 software pipeline: the gathers of nonzero u are in flight
+          // while nonzero u-1 is reduced and applied.  The loop body is
+          // straight-line, so the wait before each consume covers exactly the
+          // older pair of loads.
+          Gather<MODE, KV, LV, HAD> ga, gb;
+          float ysel = 0.f;
+          auto issue = [&](Gather<MODE, KV, LV, HAD> &g, int u) {
+            const int src = gbase + off + u;
+            const uint32_t j = (uint32_t)bperm_i(src, wj);
+            g.b = bperm_f(src, wv);
+            if constexpr (MODE != kSpmm) ldv_off<KV>(g.d, Dm, j * strideD + offD);
+            if constexpr (MODE != kSddmm) ldv_off<LV>(g.e, Em, j * strideE + offE);
+            if constexpr (HAD) ldv_off<LV>(g.h, Gm, j * strideE + offE);
+          };
+          auto consume = [&](const Gather<MODE, KV, LV, HAD> &g, int u) {
+            float y;
+            if constexpr (MODE == kSpmm) {
+              y = g.b;
+            } else {
+              float t = 0.f;
+  #pragma unroll
+              for (int v = 0; v < KV; ++v) t = fmaf(c[v], g.d[v], t);
+              t = group_sum<W>(t);
+              y = g.b * t;
+            }
+            if constexpr (MODE == kSddmm) {
+              if (glane == u) ysel = y;
+            } else if constexpr (HAD) {
+  #pragma unroll
+              for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v] * g.h[v], acc[v]);
+            } else {
+  #pragma unroll
+              for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v], acc[v]);
+            }
+          };
+          issue(ga, 0);
+          int u = 1;
+          for (; u + 1 < n; u += 2) {
+            issue(gb, u);
+            consume(ga, u - 1);
+            issue(ga, u + 1);
+            consume(gb, u);
+          }
+          if (u < n) {
+            issue(gb, u);
+            consume(ga, u - 1);
+            consume(gb, u);
+          } else {
+            consume(ga, u - 1);
+          }
+          if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
+        } else {
+          // one producer pass: sub-group `sub` forms the scalar of nonzero p+sub
+          const bool act = sub < n;
+          float y = 0.f;
+          if (MODE != kSpmm) {
+            // (lanes with sub >= n read a stale window entry and discard it)
+            const int src = (gbase + off + sub) & 63;
+            const uint32_t js = (uint32_t)bperm_i(src, wj);
+            const float bs = bperm_f(src, wv);
+            float dr[KV];
+            float t = 0.f;
+            if (act) {
+              ldv_off<KV>(dr, Dm, js * strideD + offD);
+  #pragma unroll
+              for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[v], t);
+            }
+            t = group_sum<PS>(t);
+            y = bs * t;
+            if (MODE == kSddmm && act && q == 0) out[p + sub] = y;
+          }
+          if (MODE != kSddmm && SCHED == kPaced) {
+            // consumer: the whole worker streams each E row, one row issued
+            // after the previous one has arrived
+            uint32_t jj[NB];
+            float yy[NB];
+  #pragma unroll
+            for (int u = 0; u < NB; ++u) {
+              const int src = (gbase + off + u) & 63;
+              jj[u] = (uint32_t)bperm_i(src, wj);
+              yy[u] = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f((gbase + u * PS) & 63, y);
+            }
+            float er[NB][LV];
+  #pragma unroll
+            for (int u = 0; u < NB; ++u) {
+              if (u < n) {
+                if (u > 0) wait_vmcnt<1>();
+                ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
+              }
+            }
+  #pragma unroll
+            for (int u = 0; u < NB; ++u) {
+              if (u < n) {
+  #pragma unroll
+                for (int v = 0; v < LV; ++v) acc[v] = fmaf(yy[u], er[u][v], acc[v]);
+              }
+            }
+          } else if (MODE != kSddmm) {
+            // consumer: the whole worker streams each E row, depth-2 pipeline
+            float ea[LV], eb[LV];
+            float ya = 0.f, yb = 0.f;
+            auto issue = [&](float (&e)[LV], float &yv, int u) {
+              const int src = gbase + off + u;
+              const uint32_t j = (uint32_t)bperm_i(src, wj);
+              yv = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f(gbase + u * PS, y);
+              ldv_off<LV>(e, Em, j * strideE + offE);
+            };
+            auto consume = [&](const float (&e)[LV], float yv) {
+  #pragma unroll
+              for (int v = 0; v < LV; ++v) acc[v] = fmaf(yv, e[v], acc[v]);
+            };
+            issue(ea, ya, 0);
+            int u = 1;
+            for (; u + 1 < n; u += 2) {
+              issue(eb, yb, u);
+              consume(ea, ya);
+              issue(ea, ya, u + 1);
+              consume(eb, yb);
+            }
+            if (u < n) {
+              issue(eb, yb, u);
+              consume(ea, ya);
+              consume(eb, yb);
+            } else {
+              consume(ea, ya);
+            }
+          }
+        }
+        p += n;
+      }
+  }
+};
+
+// ------------------------------------------------------ fast-path kernel
+//
+// One worker (W lanes) per merge-path slice; per row of the slice, C_i is
+// loaded once, RowWalk applies the row's nonzeros, and the row (or its
+// partial) is stored.  Besides the nonzero window of RowWalk, a rowptr
+// window (one row end per lane) keeps the row ends off the critical path.
+// C_i, the CSR arrays and A are streamed once per call and carry the
+// nontemporal hint.
+template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U>
+__global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
   const Slice s = make_slice<W>(a);
   if (!s.active) return;
+  RowWalk<MODE, W, NB, KV, LV, SCHED, U> rw(a, s.p1, (uint32_t)a.L * 4u);
+  const int glane = rw.glane, gbase = rw.gbase;
   const int64_t worker = s.id;  // carry slots and metadata are per slice
   int32_t *meta = a.meta + 2 * worker;
   const int32_t *__restrict__ rowptr = a.rowptr;
-  const int32_t *__restrict__ colidx = a.colidx;
-  const float *__restrict__ vals = a.vals;
   const float *__restrict__ Cm = a.C;
-  const float *__restrict__ Dm = a.D;
-  const float *__restrict__ Em = a.E;
   float *__restrict__ out = a.out;
   const int64_t K = a.K, L = a.L, N = a.N;
   constexpr int64_t kFar = -((int64_t)1 << 40);
-  // byte strides of D and E rows and this lane's byte offset inside a row
-  const uint32_t strideD = (uint32_t)K * 4u, strideE = (uint32_t)L * 4u;
-  const uint32_t offD = (uint32_t)(q * KV) * 4u, offE = (uint32_t)(glane * LV) * 4u;
 
   int64_t i = s.i0, p = s.p0;
   int64_t rb = kFar;  // rowptr window: wr = rowptr[rb + glane]
   int wr = 0;
-  int64_t wb = kFar;  // nonzero window: wj = colidx[wb + glane], wv = vals[wb + glane]
-  int wj = 0;
-  float wv = 0.f;
   while (true) {
     const bool has_end = i < s.i1;
     if (!has_end && i >= N) break;
@@ -362,191 +587,8 @@ __global__ __launch_bounds__(256) void walk_fast(WalkArgs a) {
     float c[KV];
 #pragma unroll
     for (int v = 0; v < KV; ++v) c[v] = 0.f;
-    if (MODE != kSpmm && p < r_end) ldv<KV, kNT>(c, Cm + i * K + q * KV);
-    while (p < r_end) {
-      if (p >= wb + W) {  // refill the nonzero window
-        wb = p;
-        const int64_t pw = wb + glane;
-        if (pw < s.p1) {
-          wj = kNT ? ld_stream(colidx + pw) : colidx[pw];
-          wv = kNT ? ld_stream(vals + pw) : vals[pw];
-        }
-      }
-      // this step: the row's nonzeros inside the window (at most NB for a
-      // producer pass of the multi-dot variant)
-      int n = (int)(r_end - p < wb + W - p ? r_end - p : wb + W - p);
-      if (NB > 1 && n > NB) n = NB;
-      if (SCHED == kPaced && n > U) n = U;
-      const int off = (int)(p - wb);
-      if constexpr (NB == 1 && SCHED == kPaced) {
-        uint32_t jj[U];
-        float bb[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {  // lanes past n read stale entries, unused
-          const int src = (gbase + off + u) & 63;
-          jj[u] = (uint32_t)bperm_i(src, wj);
-          bb[u] = bperm_f(src, wv);
-        }
-        float dr[U][KV];
-        float er[U][LV];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          if (u < n) {
-            if (u > 0) wait_vmcnt<1>();
-            if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
-            if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
-          }
-        }
-        float ysel = 0.f;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          if (u < n) {
-            float y;
-            if constexpr (MODE == kSpmm) {
-              y = bb[u];
-            } else {
-              float t = 0.f;
-#pragma unroll
-              for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[u][v], t);
-              t = group_sum<W>(t);
-              y = bb[u] * t;
-            }
-            if constexpr (MODE == kSddmm) {
-              if (glane == u) ysel = y;
-            } else {
-#pragma unroll
-              for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, er[u][v], acc[v]);
-            }
-          }
-        }
-        if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
-      } else if constexpr (NB == 1) {
-        // Depth-2 software pipeline: the gathers of nonzero u are in flight
-        // while nonzero u-1 is reduced and applied.  The loop body is
-        // straight-line, so the wait before each consume covers exactly the
-        // older pair of loads.
-        Gather<MODE, KV, LV, 0> ga, gb;
-        float ysel = 0.f;
-        auto issue = [&](Gather<MODE, KV, LV, 0> &g, int u) {
-          const int src = gbase + off + u;
-          const uint32_t j = (uint32_t)bperm_i(src, wj);
-          g.b = bperm_f(src, wv);
-          if constexpr (MODE != kSpmm) ldv_off<KV>(g.d, Dm, j * strideD + offD);
-          if constexpr (MODE != kSddmm) ldv_off<LV>(g.e, Em, j * strideE + offE);
-        };
-        auto consume = [&](const Gather<MODE, KV, LV, 0> &g, int u) {
-          float y;
-          if constexpr (MODE == kSpmm) {
-            y = g.b;
-          } else {
-            float t = 0.f;
-#pragma unroll
-            for (int v = 0; v < KV; ++v) t = fmaf(c[v], g.d[v], t);
-            t = group_sum<W>(t);
-            y = g.b * t;
-          }
-          if constexpr (MODE == kSddmm) {
-            if (glane == u) ysel = y;
-          } else {
-#pragma unroll
-            for (int v = 0; v < LV; ++v) acc[v] = fmaf(y, g.e[v], acc[v]);
-          }
-        };
-        issue(ga, 0);
-        int u = 1;
-        for (; u + 1 < n; u += 2) {
-          issue(gb, u);
-          consume(ga, u - 1);
-          issue(ga, u + 1);
-          consume(gb, u);
-        }
-        if (u < n) {
-          issue(gb, u);
-          consume(ga, u - 1);
-          consume(gb, u);
-        } else {
-          consume(ga, u - 1);
-        }
-        if (MODE == kSddmm && glane < n) out[p + glane] = ysel;
-      } else {
-        // one producer pass: sub-group `sub` forms the scalar of nonzero p+sub
-        const bool act = sub < n;
-        float y = 0.f;
-        if (MODE != kSpmm) {
-          // (lanes with sub >= n read a stale window entry and discard it)
-          const int src = (gbase + off + sub) & 63;
-          const uint32_t js = (uint32_t)bperm_i(src, wj);
-          const float bs = bperm_f(src, wv);
-          float dr[KV];
-          float t = 0.f;
-          if (act) {
-            ldv_off<KV>(dr, Dm, js * strideD + offD);
-#pragma unroll
-            for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[v], t);
-          }
-          t = group_sum<PS>(t);
-          y = bs * t;
-          if (MODE == kSddmm && act && q == 0) out[p + sub] = y;
-        }
-        if (MODE != kSddmm && SCHED == kPaced) {
-          // consumer: the whole worker streams each E row, one row issued
-          // after the previous one has arrived
-          uint32_t jj[NB];
-          float yy[NB];
-#pragma unroll
-          for (int u = 0; u < NB; ++u) {
-            const int src = (gbase + off + u) & 63;
-            jj[u] = (uint32_t)bperm_i(src, wj);
-            yy[u] = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f((gbase + u * PS) & 63, y);
-          }
-          float er[NB][LV];
-#pragma unroll
-          for (int u = 0; u < NB; ++u) {
-            if (u < n) {
-              if (u > 0) wait_vmcnt<1>();
-              ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < NB; ++u) {
-            if (u < n) {
-#pragma unroll
-              for (int v = 0; v < LV; ++v) acc[v] = fmaf(yy[u], er[u][v], acc[v]);
-            }
-          }
-        } else if (MODE != kSddmm) {
-          // consumer: the whole worker streams each E row, depth-2 pipeline
-          float ea[LV], eb[LV];
-          float ya = 0.f, yb = 0.f;
-          auto issue = [&](float (&e)[LV], float &yv, int u) {
-            const int src = gbase + off + u;
-            const uint32_t j = (uint32_t)bperm_i(src, wj);
-            yv = (MODE == kSpmm) ? bperm_f(src, wv) : bperm_f(gbase + u * PS, y);
-            ldv_off<LV>(e, Em, j * strideE + offE);
-          };
-          auto consume = [&](const float (&e)[LV], float yv) {
-#pragma unroll
-            for (int v = 0; v < LV; ++v) acc[v] = fmaf(yv, e[v], acc[v]);
-          };
-          issue(ea, ya, 0);
-          int u = 1;
-          for (; u + 1 < n; u += 2) {
-            issue(eb, yb, u);
-            consume(ea, ya);
-            issue(ea, ya, u + 1);
-            consume(eb, yb);
-          }
-          if (u < n) {
-            issue(eb, yb, u);
-            consume(ea, ya);
-            consume(eb, yb);
-          } else {
-            consume(ea, ya);
-          }
-        }
-      }
-      p += n;
-    }
+    if (MODE != kSpmm && p < r_end) ldv<KV, kNT>(c, Cm + i * K + rw.q * KV);
+    rw.row(p, r_end, c, acc);
     if constexpr (MODE != kSddmm) {
       if (!has_end) stv<LV>(a.carry + (worker * 2 + 1) * (int64_t)a.Lw + glane * LV, acc);
       else if (i == s.i0 && s.head) stv<LV>(a.carry + (worker * 2) * (int64_t)a.Lw + glane * LV, acc);
