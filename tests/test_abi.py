@@ -148,3 +148,13 @@ def test_next_entry_points_argument_errors():
     assert L.sparselnr_fused_sddmm_spmm_dt(*(FAKE,) * 4, NULL, FAKE, FAKE, 4, 4, 4, 4, NULL) == \
         slnr.ERR_INVALID_ARG
     assert L.sparselnr_fused_sddmm_spmm_dt(*(FAKE,) * 7, -4, 4, 4, 4, NULL) == slnr.ERR_INVALID_ARG
+
+
+def test_header_is_plain_c(tmp_path):
+    """The header and the C caller compile as C11 (no C++ in the interface)."""
+    import subprocess
+    src = os.path.join(ROOT, "tests", "c_abi", "abi_check.c")
+    r = subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-fsyntax-only",
+                        "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"), src],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr

@@ -1,0 +1,22 @@
+"""The C ABI from a plain C program (tests/c_abi/abi_check.c): HIP C runtime
+allocations, the fused and unfused entry points, status codes, and every row
+checked against the oracle's C entry point with the parity rule."""
+import os
+import subprocess
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+EXE = os.path.join(ROOT, "tests", "c_abi", "abi_check")
+
+
+def test_plain_c_caller(gpu):
+    if not os.path.exists(EXE):
+        pytest.fail("%s is not built: run __graft_entry__.build()" % EXE)
+    print("running", EXE, flush=True)
+    r = subprocess.run([EXE], capture_output=True, text=True, timeout=120)
+    print(r.stdout, r.stderr, flush=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "abi_check: ok" in r.stdout
