@@ -139,7 +139,7 @@ def make_workload(kernel, config, dev):
             bytes=csr_bytes + 4 * nnz * (K + L) + 4 * N * K + 4 * N * Mo + 4 * L * Mo,
             bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N Mo + 4 L Mo",
             footprint=csr_bytes + 4 * (N * K + M * K + M * L + L * Mo + N * Mo),
-            dominant="walk_fast fused with per-row GEMV epilogue + carry_fixup (one call)",
+            dominant="walk_epi fused with matrix-core epilogue + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").sddmm_spmm_gemm_rows(
                 base.rowptr, base.colidx, base.vals, Ch, Dh, Fh, Wh))
 
@@ -165,7 +165,7 @@ def make_workload(kernel, config, dev):
             bytes=csr_bytes + 4 * nnz * K + 4 * K * L + 4 * N * L,
             bytes_model="4(N+1) + 8 nnz + 4 nnz K + 4 K L + 4 N L",
             footprint=csr_bytes + 4 * (M * K + K * L + N * L),
-            dominant="walk_fast SpMM with per-row GEMV epilogue + carry_fixup (one call)",
+            dominant="walk_epi SpMM with matrix-core epilogue + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").spmm_gemm_rows(base.rowptr, base.colidx,
                                                                base.vals, Ch, Dh))
 
@@ -184,6 +184,9 @@ def make_workload(kernel, config, dev):
             slnr.sparselnr_spmm(rp, ci, v, H, T, stream=stream)
             torch.mm(T, E, out=A2)
         w.update(J=J, L=L)
+        # the library forms C .* D once when nnz >= 3 M (12 M J bytes, then
+        # one gathered row per nonzero), else per nonzero from two rows
+        hoisted = nnz >= 3 * M
         return dict(
             metric="fused <SpMMH,GEMM> Gnnz/s + achieved HBM GB/s vs peak, %s J=L=128" % config,
             desc=desc, sizes=w,
@@ -191,11 +194,14 @@ def make_workload(kernel, config, dev):
             compare=two_pass,
             compare_desc="torch.mul C .* D into an M x J temporary, sparselnr_spmm into an "
                          "N x J temporary, then torch.mm by E",
-            bytes=csr_bytes + 8 * nnz * J + 4 * J * L + 4 * N * L,
-            bytes_model="4(N+1) + 8 nnz + 8 nnz J + 4 J L + 4 N L",
-            footprint=csr_bytes + 4 * (2 * M * J + J * L + N * L),
-            dominant="walk_fast Hadamard SpMM with per-row GEMV epilogue + carry_fixup "
-                     "(one call)",
+            bytes=(12 * M * J + csr_bytes + 4 * nnz * J + 4 * J * L + 4 * N * L) if hoisted
+            else (csr_bytes + 8 * nnz * J + 4 * J * L + 4 * N * L),
+            bytes_model="12 M J + 4(N+1) + 8 nnz + 4 nnz J + 4 J L + 4 N L (C .* D formed once)"
+            if hoisted else "4(N+1) + 8 nnz + 8 nnz J + 4 J L + 4 N L (C .* D per nonzero)",
+            footprint=csr_bytes + 4 * ((3 if hoisted else 2) * M * J + J * L + N * L),
+            dominant="hadamard4_kernel + walk_epi SpMM with matrix-core epilogue + carry_fixup "
+                     "(one call)" if hoisted else
+                     "walk_epi Hadamard SpMM with matrix-core epilogue + carry_fixup (one call)",
             oracle=lambda: __import__("oracle").spmmh_gemm_rows(base.rowptr, base.colidx,
                                                                 base.vals, Ch, Dh, Eh))
 

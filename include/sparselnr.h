@@ -162,6 +162,13 @@ SPARSELNR_API int sparselnr_spmm_gemm(const int32_t *rowptr, const int32_t *coli
  * followed by A_i = t_i E.  B is N x M; C, D: M x J; E: J x L; A: N x L.
  * Supported: J in {16, 32, 64, 128, 256, 512}, any L; C and D 16-byte
  * aligned.
+ * C .* D does not depend on the row i.  When nnz >= 3 M (decided on the
+ * device, which alone knows nnz) it is formed once into a per-(device,
+ * stream) workspace of M x J floats and gathered as one row per nonzero;
+ * otherwise each nonzero multiplies its two gathered rows.  Both schedules
+ * round the same products in the same order, so A is bit-identical either
+ * way.  The workspace is allocated on the first call of a shape (failure:
+ * SPARSELNR_ERR_NO_MEMORY) and freed by sparselnr_release().
  */
 SPARSELNR_API int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx,
                                        const float *vals, const float *C, const float *D,

@@ -46,6 +46,7 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
   float *tile = smem + wave * (TR * TS);
   uint64_t *tdst = reinterpret_cast<uint64_t *>(smem + (blockDim.x >> 6) * (TR * TS)) + wave * TR;
 
+  if (gate_closed(a.gate, a.rowptr, a.N, a.gate_nnz)) return;
   const Slice s = make_slice<W>(a);
   const int64_t worker = s.id;
   RowWalk<MODE, W, 1, KV, LV, SCHED, U, HAD> rw(a, s.p1, (uint32_t)LIN * 4u);

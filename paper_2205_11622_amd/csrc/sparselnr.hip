@@ -33,6 +33,9 @@ constexpr int kXcds = 8;          // MI355X deals blocks over 8 XCDs
 #endif
 constexpr int kGridFactor = SLNR_GRID_FACTOR;
 constexpr int kGenericLT = 4;     // generic path: 4 x 64 = 256 columns per tile
+// <SpMMH, GEMM>: C .* D is formed once when nnz >= kHoistRatio * M (12 M J
+// bytes for the product against 4 J bytes per nonzero for a second gather).
+constexpr int64_t kHoistRatio = 3;
 
 int hip_fail(hipError_t e) {
   g_last_hip_error = (int)e;
@@ -308,16 +311,47 @@ Grid make_grid(int cus, int per_cu, int block, int W, int64_t N) {
   return g;
 }
 
+// Launch shape of the carry fixup: each wave takes groups of G slices, G
+// the smallest power of two from 8 to 64 that covers all `workers` slices
+// with at most 32 waves per CU.
+struct FixupShape {
+  int blocks;
+  int G;
+};
+
+FixupShape fixup_shape(int cus, int64_t workers) {
+  const int64_t max_waves = (int64_t)cus * 32;
+  int G = 8;
+  while (G < 64 && (workers + G - 1) / G > max_waves) G *= 2;
+  const int64_t waves = (workers + G - 1) / G;
+  int64_t blocks = (waves + (kBlock / 64) - 1) / (kBlock / 64);
+  if (blocks > max_waves / (kBlock / 64)) blocks = max_waves / (kBlock / 64);
+  return FixupShape{(int)(blocks > 0 ? blocks : 1), G};
+}
+
 // Runs one merge-path walk (+ carry fixup unless SDDMM) over the whole matrix.
-int run_walk(Mode mode, const Variant &v0, WalkArgs a, hipStream_t stream) {
+// With nv > 1, the variants are gated alternatives, each with its own
+// arguments as[k] (only the one whose gate opens on the device does any
+// work): they share one grid, workspace and slice split, so the one carry
+// fixup serves whichever ran.
+int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream_t stream) {
+  WalkArgs a = as[0];
   int dev = 0, cus = 0, rc;
   if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
   if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
-  Variant v = v0;
+  Variant v = vs[0];
   int per_cu = 1;
   if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
+  for (int t = 1; t < nv; ++t) {
+    if (vs[t].W != v.W || vs[t].block != v.block || vs[t].generic != v.generic)
+      return SPARSELNR_ERR_UNSUPPORTED;  // alternatives must split the matrix alike
+    int pc = 1;
+    if ((rc = blocks_per_cu(dev, vs[t].fn, vs[t].block, vs[t].lds, &pc)) != SPARSELNR_OK)
+      return rc;
+    if (pc < per_cu) per_cu = pc;
+  }
   Grid g = make_grid(cus, per_cu, v.block, v.W, a.N);
-  if (g.factor == 1 && v.fn_small) {  // one resident grid: take the small-input schedule
+  if (nv == 1 && g.factor == 1 && v.fn_small) {  // one resident grid: the small-input schedule
     v.fn = v.fn_small;
     if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
     g = make_grid(cus, per_cu, v.block, v.W, a.N);
@@ -343,17 +377,33 @@ int run_walk(Mode mode, const Variant &v0, WalkArgs a, hipStream_t stream) {
   for (int64_t t = 0; t < (mode == kSddmm ? 1 : tiles); ++t) {
     a.l0 = (int32_t)(t * tile_w);
     a.Lw = (int32_t)((a.L - a.l0) < tile_w ? (a.L - a.l0) : tile_w);
-    hipLaunchKernelGGL(v.fn, dim3(g.blocks), dim3(v.block), v.lds, stream, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e);
+    for (int k = 0; k < nv; ++k) {
+      WalkArgs ak = as[k];  // the shared fields come from a
+      ak.workers = a.workers;
+      ak.min_chunk = a.min_chunk;
+      ak.xcd_span = a.xcd_span;
+      ak.xcds = a.xcds;
+      ak.carry = a.carry;
+      ak.meta = a.meta;
+      ak.l0 = a.l0;
+      ak.Lw = a.Lw;
+      hipLaunchKernelGGL(k == 0 ? v.fn : vs[k].fn, dim3(g.blocks), dim3(vs[k].block),
+                         vs[k].lds, stream, ak);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return hip_fail(e);
+    }
     if (mode != kSddmm) {
-      const int fix_blocks = (g.workers + (kBlock / 64) - 1) / (kBlock / 64);
-      hipLaunchKernelGGL(slnr::carry_fixup, dim3(fix_blocks), dim3(kBlock), 0, stream, a);
-      e = hipGetLastError();
+      const FixupShape fs = fixup_shape(cus, g.workers);
+      hipLaunchKernelGGL(slnr::carry_fixup, dim3(fs.blocks), dim3(kBlock), 0, stream, a, fs.G);
+      hipError_t e = hipGetLastError();
       if (e != hipSuccess) return hip_fail(e);
     }
   }
   return SPARSELNR_OK;
+}
+
+int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
+  return run_walk(mode, &v, &a, 1, stream);
 }
 
 bool bad_size(int64_t N, int64_t M, int64_t K, int64_t L) {
@@ -380,6 +430,8 @@ WalkArgs base_args(const int32_t *rowptr, const int32_t *colidx, const float *va
   a.Lin = (int32_t)L;
   a.G2 = nullptr;
   a.Wep = nullptr;
+  a.gate_nnz = 0;
+  a.gate = slnr::kGateNone;
   return a;
 }
 
@@ -540,8 +592,46 @@ int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx, const flo
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
   if (!(aligned16(C) && aligned16(D) && offsets32(M, J))) return SPARSELNR_ERR_UNSUPPORTED;
-  return run_epilogue(kSpmm, true, rowptr, colidx, vals, nullptr, nullptr, C, D, E, A, N, 0, J,
-                      L, stream);
+  Variant vs[2] = {pick_epi<kSpmm, 0>(J), pick_epi<kSpmm, 1>(J)};
+  if (!vs[0].fn || !vs[1].fn) return SPARSELNR_ERR_UNSUPPORTED;
+  if (M == 0 || J == 0)  // no rows to gather: the per-nonzero form alone
+    return run_epilogue(kSpmm, true, rowptr, colidx, vals, nullptr, nullptr, C, D, E, A, N, 0, J,
+                        L, stream);
+  // C .* D does not depend on the row, so it can be formed once (M x J,
+  // 12 M J bytes) and gathered as one row per nonzero, or formed per nonzero
+  // from two gathered rows (4 J more bytes per nonzero).  The first moves
+  // fewer bytes when nnz >= 3 M.  nnz is known on the device only, so both
+  // schedules are launched, gated on it, and exactly one of them runs.
+  int dev = 0;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  void *ws = nullptr;
+  if ((rc = get_workspace(dev, s, (size_t)M * J * sizeof(float), &ws, 2)) != SPARSELNR_OK)
+    return rc;
+  float *H = (float *)ws;
+  const int64_t gate_nnz = kHoistRatio * M;
+  int cus = 0;
+  if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
+  const int64_t n4 = M * J / 4;  // J is a multiple of 4 (supported widths)
+  int64_t hb = (n4 + kBlock - 1) / kBlock;
+  if (hb > (int64_t)cus * 8) hb = (int64_t)cus * 8;
+  hipLaunchKernelGGL(slnr::hadamard4_kernel, dim3((unsigned)hb), dim3(kBlock), 0, s, C, D, H, n4,
+                     rowptr, N, gate_nnz, (int)slnr::kGateDense);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e);
+  WalkArgs as[2];
+  as[0] = base_args(rowptr, colidx, vals, N, 0, L);
+  as[0].Wep = E;
+  as[0].Lin = (int32_t)J;
+  as[0].out = A;
+  as[0].gate_nnz = gate_nnz;
+  as[1] = as[0];
+  as[0].E = H;  // hoisted: one gathered row of H = C .* D per nonzero
+  as[0].gate = slnr::kGateDense;
+  as[1].E = C;  // per nonzero: C_k .* D_k from two gathered rows
+  as[1].G2 = D;
+  as[1].gate = slnr::kGateSparse;
+  return run_walk(kSpmm, vs, as, 2, s);
 }
 
 int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,

@@ -78,7 +78,22 @@ struct WalkArgs {
   int32_t Lin;        // width of the gathered consumer rows (E, G2); == L without epilogue
   const float *G2;    // second gathered row source, multiplied elementwise (M x Lin)
   const float *Wep;   // per-row epilogue matrix (Lin x L): A_i = t_i * Wep
+  // Gate of a launch whose schedule depends on nnz, which only the device
+  // knows: kGateNone runs always, kGateDense only if nnz >= gate_nnz,
+  // kGateSparse only if nnz < gate_nnz.  A closed launch exits at once.
+  int64_t gate_nnz;
+  int32_t gate;
 };
+
+enum Gate : int { kGateNone = 0, kGateDense = 1, kGateSparse = 2 };
+
+// True when the gate of this launch is closed (uniform over the grid).
+__device__ __forceinline__ bool gate_closed(int gate, const int32_t *rowptr, int64_t N,
+                                            int64_t gate_nnz) {
+  if (gate == kGateNone) return false;
+  const bool dense = (int64_t)rowptr[N] >= gate_nnz;
+  return gate == kGateDense ? !dense : dense;
+}
 
 // ---------------------------------------------------------------- lane ops
 
@@ -669,24 +684,24 @@ __global__ __launch_bounds__(256) void walk_generic(WalkArgs a) {
 
 // ------------------------------------------------------------ carry fixup
 //
-// One wave per worker slice.  A slice whose first row is a head row (begun
-// by earlier slices) adds, in slice order, the tail partials of the earlier
-// slices that end inside that row, then its own head partial, and writes
-// the row of A.
-__global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
-  const float *__restrict__ carry = a.carry;
-  const int32_t *__restrict__ meta = a.meta;
-  float *__restrict__ A = a.out;
-  const int64_t Lw = a.Lw, L = a.L, l0 = a.l0;
+// A slice whose first row is a head row (begun by earlier slices) owns that
+// row's fixup: it adds, in slice order, the tail partials of the earlier
+// slices that end inside the row, then its own head partial, and writes the
+// row of A.  Each wave takes groups of G consecutive slices (G a power of
+// two up to 64, grid-stride): lanes 0..G-1 read the group's head entries at
+// once and the wave then fixes the group's head rows one after another.  The
+// host picks G so that the grid holds at most 32 waves per CU: a call on a
+// small matrix does not pay for one wave per possible slice, and a power-law
+// matrix, where a large share of the slices start inside a long row, still
+// spreads its head rows over many waves.
+
+// The run of slices [first, c) whose tail row is r (they are contiguous and
+// end at c - 1), found with one ballot per 64 slices.  Uniform in the wave.
+__device__ __forceinline__ int64_t tail_run_start(const int32_t *__restrict__ meta, int64_t c,
+                                                  int32_t r) {
   const int lane = threadIdx.x & 63;
-  const int64_t c = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
-  int64_t S, ns, items, nnz;
-  slice_count(a, &S, &ns, &items, &nnz);
-  if (c >= ns) return;
-  const int32_t r = meta[2 * c + 1];
-  if (r < 0) return;
   int64_t first = c;
-  while (true) {  // slices with tail row r are contiguous and end at c - 1
+  while (true) {
     const int64_t idx = first - 1 - lane;
     const bool same = idx >= 0 && meta[2 * idx] == r;
     const uint64_t m = __ballot(same);
@@ -694,9 +709,18 @@ __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
     first -= run;
     if (run < 64) break;
   }
-  // Sum in slice order.  The loads of a batch are issued together, so a row
-  // split over hundreds of slices (a power-law hub row) costs a few memory
-  // latencies rather than one per slice; the adds stay in slice order.
+  return first;
+}
+
+// Lanes over columns, partials summed in slice order.  The loads of a batch
+// are issued together, so a row split over hundreds of slices (a power-law
+// hub row) costs a few memory latencies rather than one per slice.
+__device__ __forceinline__ void fix_row(const WalkArgs &a, int64_t c, int32_t r) {
+  const float *__restrict__ carry = a.carry;
+  float *__restrict__ A = a.out;
+  const int64_t Lw = a.Lw, L = a.L, l0 = a.l0;
+  const int lane = threadIdx.x & 63;
+  const int64_t first = tail_run_start(a.meta, c, r);
   constexpr int kBatch = 16;
   for (int64_t l = lane; l < Lw; l += 64) {
     float sum = 0.f;
@@ -719,6 +743,48 @@ __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a) {
     }
     sum += carry[(c * 2) * Lw + l];
     A[(int64_t)r * L + l0 + l] = sum;
+  }
+}
+
+__global__ __launch_bounds__(256) void carry_fixup(WalkArgs a, int G) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+  int64_t S, ns, items, nnz;
+  slice_count(a, &S, &ns, &items, &nnz);
+  // meta entries past ns belong to no slice of this call and are never read
+  for (int64_t g0 = wave * G; g0 < ns; g0 += waves * G) {
+    const int64_t cl = g0 + lane;
+    const int32_t rl = (lane < G && cl < ns) ? a.meta[2 * cl + 1] : -1;
+    uint64_t heads = __ballot(rl >= 0);
+    while (heads) {  // wave-uniform
+      const int b = __builtin_ctzll(heads);
+      heads &= heads - 1;
+      fix_row(a, g0 + b, bperm_i(b, rl));
+    }
+  }
+}
+
+// ------------------------------------------------------------ Hadamard
+//
+// H = C .* D elementwise over n4 float4 elements (16-byte aligned arrays),
+// grid-stride.  C and D are streamed once (nontemporal); H is stored plainly
+// because the walk that follows gathers it.  Gated like the walks: the
+// launch does nothing unless its gate is open.
+__global__ __launch_bounds__(256) void hadamard4_kernel(const float *__restrict__ C,
+                                                        const float *__restrict__ D,
+                                                        float *__restrict__ H, int64_t n4,
+                                                        const int32_t *rowptr, int64_t N,
+                                                        int64_t gate_nnz, int gate) {
+  if (gate_closed(gate, rowptr, N, gate_nnz)) return;
+  const f4_t *c4 = reinterpret_cast<const f4_t *>(C);
+  const f4_t *d4 = reinterpret_cast<const f4_t *>(D);
+  f4_t *h4 = reinterpret_cast<f4_t *>(H);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n4; t += stride) {
+    const f4_t x = __builtin_nontemporal_load(c4 + t);
+    const f4_t y = __builtin_nontemporal_load(d4 + t);
+    h4[t] = x * y;
   }
 }
 

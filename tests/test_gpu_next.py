@@ -69,6 +69,58 @@ def test_spmmh_gemm(gpu, J, L):
     assert_rows_close(rows_of(A, None), ref, scale)
 
 
+@pytest.mark.parametrize("J,L", [(16, 3), (32, 32), (64, 17), (128, 128), (256, 64),
+                                 (512, 128)])
+def test_spmmh_gemm_per_nonzero_schedule(gpu, J, L):
+    """Fewer than 3 nonzeros per column of B (nnz < 3 M): the library forms
+    C_k .* D_k per nonzero from two gathered rows instead of forming C .* D
+    once."""
+    n = power_law_lengths(3000, seed=J + L, scale=1.0, cap=60)
+    M = max(3000, int(n.sum()) // 3 + 1)
+    p = make_problem(n, M, J, J, seed=J + 5 * L, dense="normal")
+    assert p.nnz < 3 * M
+    C, D = p.D, p.E
+    E = synth.normal(7, 9, (J, L))
+    A = slnr.sparselnr_spmmh_gemm(*csr(p), dev(C), dev(D), dev(E))
+    ref, scale, _ = oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, C, D, E)
+    assert_rows_close(rows_of(A, None), ref, scale)
+
+
+@pytest.mark.parametrize("J", [16, 128, 512])
+def test_spmmh_gemm_schedules_agree_bitwise(gpu, J):
+    """The two schedules of <SpMMH, GEMM> (C .* D formed once when nnz >= 3 M,
+    per nonzero otherwise) round the same products in the same order, so
+    padding C and D with unused rows (which moves nnz below 3 M and switches
+    the schedule) must not change a bit of A."""
+    import torch
+    p = make_problem(lengths(J), 1500, J, J, seed=3 * J, dense="normal")
+    assert p.nnz >= 3 * p.M
+    C, D = p.D, p.E
+    E = dev(synth.normal(8, 9, (J, 96)))
+    A1 = slnr.sparselnr_spmmh_gemm(*csr(p), dev(C), dev(D), E).clone()
+    pad = p.nnz // 3 + 1 - p.M
+    Cp = np.vstack([C, synth.normal(9, 9, (pad, J))])
+    Dp = np.vstack([D, synth.normal(9, 10, (pad, J))])
+    assert p.nnz < 3 * Cp.shape[0]
+    A2 = slnr.sparselnr_spmmh_gemm(*csr(p), dev(Cp), dev(Dp), E)
+    assert torch.equal(A1.view(torch.int32), A2.view(torch.int32))
+
+
+def test_spmmh_gemm_schedule_threshold(gpu):
+    """nnz exactly 3 M takes the formed-once schedule, 3 M - 1 the other;
+    both match the oracle."""
+    J, M = 64, 400
+    for nnz in (3 * M, 3 * M - 1):
+        n = np.full(nnz // 3, 3, np.int64)
+        n[: nnz - n.sum()] += 1
+        p = make_problem(n, M, J, J, seed=nnz, dense="normal")
+        assert p.nnz == nnz
+        E = synth.normal(2, 9, (J, 40))
+        A = slnr.sparselnr_spmmh_gemm(*csr(p), dev(p.D), dev(p.E), dev(E))
+        ref, scale, _ = oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, p.E, E)
+        assert_rows_close(rows_of(A, None), ref, scale)
+
+
 @pytest.mark.parametrize("K,L", [(32, 32), (128, 128), (16, 256), (3, 5), (64, 64)])
 def test_transposed_D(gpu, K, L):
     p = make_problem(lengths(K + L), 2200, K, L, seed=K + 7 * L, dense="normal")

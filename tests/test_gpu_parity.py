@@ -78,7 +78,7 @@ def test_no_nonzeros_gives_zero_rows(gpu, K, L):
     assert bool((A == 0).all())
 
 
-@pytest.mark.parametrize("K,L", [(128, 128), (16, 256), (64, 64), (9, 9)])
+@pytest.mark.parametrize("K,L", [(128, 128), (16, 256), (64, 64), (32, 32), (9, 9)])
 def test_one_dense_row(gpu, K, L):
     # a single row holding every column: the row is split over all workers
     p = make_problem([100_000], 100_000, K, L, seed=2, dense="normal")
@@ -87,6 +87,20 @@ def test_one_dense_row(gpu, K, L):
     Y, Au = unfused(d)
     check_Y(p, Y)
     check_A_rows(p, Au)
+
+
+@pytest.mark.parametrize("L", [16, 32, 512, 12])
+def test_one_dense_row_spmm_widths(gpu, L):
+    # the SpMM alone on one row split over every worker, at the narrowest and
+    # widest fast widths and at a width with no fast variant
+    import torch
+    p = make_problem([0, 60_000, 3], 60_000, 4, L, seed=L, dense="normal")
+    d = upload(p)
+    Y = torch.from_numpy(np.ascontiguousarray(p.vals)).to(gpu)
+    A = slnr.sparselnr_spmm(d["rowptr"], d["colidx"], Y, d["E"])
+    ref, scale, _ = oracle.spmm(p.rowptr, p.colidx, p.vals, p.E, Yabs=np.abs(p.vals))
+    from tests.parity import assert_rows_close
+    assert_rows_close(A.cpu().numpy(), ref, scale)
 
 
 @pytest.mark.parametrize("K,L", [(32, 32), (128, 128)])

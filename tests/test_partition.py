@@ -215,3 +215,43 @@ def test_xcd_slice_assignment_is_a_bijection(blocks, wpb, ns):
             if in_xcd < per_xcd and sid < ns:
                 seen.append(sid)
     assert sorted(seen) == list(range(ns))
+
+
+def fixup_shape(cus, workers):
+    """Host model of the library's fixup_shape()."""
+    max_waves = cus * 32
+    G = 8
+    while G < 64 and -(-workers // G) > max_waves:
+        G *= 2
+    waves = -(-workers // G)
+    blocks = min(-(-waves // 4), max_waves // 4)
+    return max(blocks, 1), G
+
+
+@pytest.mark.parametrize("ns,workers,cus", [(1, 64, 256), (63, 64, 1), (64, 64, 1), (65, 128, 1),
+                                            (352, 65536, 256), (65536, 65536, 256),
+                                            (1000, 262144, 256), (131072, 131072, 4),
+                                            (129, 200, 1), (5000, 5000, 2)])
+def test_fixup_groups_visit_each_head_once(ns, workers, cus):
+    """Host model of carry_fixup's iteration: with G slices per group, wave w
+    takes the groups starting at w*G, (w + waves)*G, ...; within a group it
+    visits the slices whose head entry is set, in ascending order.  Every
+    head slice below ns is visited exactly once and no slice >= ns is read."""
+    blocks, G = fixup_shape(cus, workers)
+    assert G in (8, 16, 32, 64) and blocks * 4 <= max(cus * 32, 4)
+    waves = blocks * 4
+    rng = np.random.default_rng(ns * 7 + workers)
+    head = np.full(workers + 64, -1)
+    head[:ns] = np.where(rng.random(ns) < 0.3, rng.integers(0, 1000, ns), -1)
+    head[ns:] = 5  # stale entries of earlier calls: must never be used
+    visits = np.zeros(workers + 64, dtype=int)
+    for w in range(waves):
+        g0 = w * G
+        while g0 < ns:
+            flags = [lane < G and (g0 + lane < ns) and head[g0 + lane] >= 0 for lane in range(64)]
+            for b in range(64):
+                if flags[b]:
+                    visits[g0 + b] += 1
+            g0 += waves * G
+    assert np.array_equal(visits[:ns], (head[:ns] >= 0).astype(int))
+    assert not visits[ns:].any()
