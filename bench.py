@@ -399,7 +399,7 @@ def main() -> int:
             times.append(time.perf_counter() - s0)
         cs = float(np.median(times))
         cpu = {"value": round(nnz / cs / 1e9, 6), "unit": "Gnnz/s", "cores": oracle.num_threads(),
-               "kind": "oracle", "seconds": round(cs, 3), "passes": len(times),
+               "kind": "oracle", "seconds": float("%.4g" % cs), "passes": len(times),
                "sample": "the whole %s workload (%d rows, %d nonzeros) per pass, median of %d "
                          "passes, fp64 accumulation, OpenMP over rows"
                          % (key, wl["sizes"]["N"], nnz, len(times))}
