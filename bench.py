@@ -24,10 +24,11 @@ paper uses for it:
   spmmh_gemm       A = (B (C .* D)) E,      C, D are M x 128, E is 128 x 128
   dt               <SDDMM, SpMM> with D stored transposed (K x M), K = L = 128
 
---sweep (with --kernel spmm_gemm) instead prints one JSON line per (K, L) in
-{16, 32, 64, 128, 256, 512}^2: the fused call against the separate passes
-(SpMM into an N x K temporary, then torch.mm), the inner-size study of the
-paper's Section 6.3 (Figure 8) on the --config sparsity structure.
+--sweep instead prints one JSON line per (K, L) in {16, 32, 64, 128, 256,
+512}^2 on the --config sparsity structure, the fused call against the
+separate passes: with --kernel spmm_gemm, SpMM into an N x K temporary then
+torch.mm (the inner-size study of the paper's Section 6.3, Figure 8); with
+--kernel sddmm_spmm, the library's unfused SDDMM then SpMM.
 """
 from __future__ import annotations
 
@@ -276,6 +277,48 @@ def sweep_spmm_gemm(args, dev, timed) -> None:
         torch.cuda.empty_cache()
 
 
+def sweep_sddmm_spmm(args, dev, timed) -> None:
+    """Fused <SDDMM, SpMM> against the library's unfused passes over K, L in
+    {16..512} on the --config sparsity structure: where fusion pays on this GPU."""
+    import numpy as np
+    import torch
+
+    import paper_2205_11622_amd as slnr
+    import synth
+
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)  # noqa: E731
+    stream = torch.cuda.current_stream(dev)
+    base = synth.config(args.config)
+    N, M, nnz = base.N, base.M, base.nnz
+    rp, ci, v = t(base.rowptr), t(base.colidx), t(base.vals)
+    Y = torch.empty(nnz, dtype=torch.float32, device=dev)
+    top = max(SWEEP_SIZES)
+    cmax, dmax, emax = (t(synth.normal(0, s, (n, top))) for s, n in ((3, N), (4, M), (5, M)))
+    for K in SWEEP_SIZES:
+        C, D = cmax[:, :K].contiguous(), dmax[:, :K].contiguous()
+        for L in SWEEP_SIZES:
+            E = emax[:, :L].contiguous()
+            A = torch.empty((N, L), dtype=torch.float32, device=dev)
+            A2 = torch.empty_like(A)
+            _, f_ms, _ = timed(lambda: slnr.sparselnr_fused_sddmm_spmm(
+                rp, ci, v, C, D, E, A, stream=stream), args.steps, args.warmup)
+            _, u_ms, _ = timed(lambda: slnr.sparselnr_unfused_sddmm_spmm(
+                rp, ci, v, C, D, E, Y, A2, stream=stream), args.steps, args.warmup)
+            f_ms /= args.steps
+            u_ms /= args.steps
+            model = 4 * (N + 1) + 8 * nnz + 4 * nnz * (K + L) + 4 * N * K + 4 * N * L
+            gbs = model / (f_ms * 1e-3) / 1e9
+            print(json.dumps({"sweep": "sddmm_spmm", "config": args.config, "K": K, "L": L,
+                              "fused_ms": round(f_ms, 5), "unfused_ms": round(u_ms, 5),
+                              "speedup": round(u_ms / f_ms, 4), "fused_GBps": round(gbs, 1),
+                              "frac": round(gbs / HBM_PEAK_GBPS, 4),
+                              "bytes_model": "4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L"}),
+                  flush=True)
+            del A, A2, E
+        del C, D
+        torch.cuda.empty_cache()
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -287,8 +330,8 @@ def main() -> int:
     ap.add_argument("--no-unfused", action="store_true",
                     help="skip the in-run comparison with the separate-pass computation")
     ap.add_argument("--sweep", action="store_true",
-                    help="with --kernel spmm_gemm: fused vs separate passes over K, L in "
-                         "{16..512} (one JSON line per point)")
+                    help="with --kernel sddmm_spmm or spmm_gemm: the fused call against the "
+                         "separate passes over K, L in {16..512} (one JSON line per point)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -330,10 +373,13 @@ def main() -> int:
         return per, ev[0].elapsed_time(ev[steps]), wall
 
     if args.sweep:
-        if args.kernel != "spmm_gemm":
-            print("--sweep is defined for --kernel spmm_gemm", file=sys.stderr)
+        if args.kernel == "spmm_gemm":
+            sweep_spmm_gemm(args, dev, timed)
+        elif args.kernel == "sddmm_spmm":
+            sweep_sddmm_spmm(args, dev, timed)
+        else:
+            print("--sweep is defined for --kernel sddmm_spmm and spmm_gemm", file=sys.stderr)
             return 2
-        sweep_spmm_gemm(args, dev, timed)
         return 0
 
     t0 = time.time()

@@ -201,11 +201,69 @@ Variant with_small(Variant v, KernelFn small) {
   return v;
 }
 
-// Fast variants exist for the widths of the benchmark workloads: K = L in
-// {32, 64, 128, 256} (one 16-byte slice of C/D and of E/A per lane) and the
-// asymmetric K = 16, L = 256 (4-lane dot products, 16 per producer pass);
-// the SpMM alone also at L = 16 and 512 (the widths of the <SpMM, GEMM>
-// sweep).
+// Lane mapping of a fused fast variant for K, L in {16, ..., 512}: the
+// consumer spreads E_j / A_i over W lanes of LV floats (L = W * LV); the
+// producer forms NB dot products per pass, each over PS = W / NB lanes of KV
+// floats (K = PS * KV).  LV is 4 (8 at L = 512) unless K is so wide against
+// L that a dot over all W lanes would need more than 16 floats per lane;
+// then the consumer takes 2 or 1 floats per lane on more lanes.  KV is 4
+// where it fits, larger when K is wide against L (one dot per pass over the
+// whole worker, at most 32 floats), 2 when 4 would need more than 64
+// registers of gathered E rows per pass.  U: nonzeros per paced step (NB for
+// the multi-dot passes, else as many as 64 registers of gathered rows allow,
+// at most 4).  W == 0: no fast variant.
+struct FusedMap {
+  int W, LV, KV, NB, U;
+};
+
+constexpr FusedMap fused_map(int K, int L) {
+  int LV = L == 512 ? 8 : 4;
+  while (LV > 1 && K / (L / LV) > 16) LV /= 2;
+  const int W = L / LV;
+  if (W > 64) return FusedMap{0, 0, 0, 0, 0};
+  int KV = 4;
+  while (KV <= 32 && K / KV > W) KV *= 2;
+  if (KV > 32) return FusedMap{0, 0, 0, 0, 0};
+  int PS = K / KV;
+  int NB = W / PS;
+  if (NB * LV > 64) {
+    KV = 2;
+    PS = K / KV;
+    NB = W / PS;
+  }
+  if (PS < 1 || PS > W || NB * PS != W || NB * LV > 64) return FusedMap{0, 0, 0, 0, 0};
+  const int fit = 64 / (KV + LV);
+  const int U = NB > 1 ? NB : (fit < 1 ? 1 : (fit < 4 ? fit : 4));
+  return FusedMap{W, LV, KV, NB, U};
+}
+
+template <int K, int L>
+Variant fused_fast() {
+  constexpr FusedMap m = fused_map(K, L);
+  if constexpr (m.W == 0) {
+    return generic<kFused>();
+  } else {
+    return fast<kFused, m.W, m.NB, m.KV, m.LV, kFS, m.U>();
+  }
+}
+
+template <int K>
+Variant fused_fast_l(int64_t L) {
+  switch (L) {
+    case 16: return fused_fast<K, 16>();
+    case 32: return fused_fast<K, 32>();
+    case 64: return fused_fast<K, 64>();
+    case 128: return fused_fast<K, 128>();
+    case 256: return fused_fast<K, 256>();
+    case 512: return fused_fast<K, 512>();
+    default: return generic<kFused>();
+  }
+}
+
+// Fast variants exist for every K, L in {16, 32, 64, 128, 256, 512}, with
+// 16-byte aligned operands.  The widths of the benchmark workloads (K = L = 32, 64,
+// 128, 256 and K = 16, L = 256) keep their measured schedules; other
+// widths take the mapping of fused_map.
 Variant pick_fused(int64_t K, int64_t L, bool al) {
   if (al) {
     if (K == 32 && L == 32) return with_small(fast<kFused, 8, 1, 4, 4, kFS, kPU>(),
@@ -215,6 +273,15 @@ Variant pick_fused(int64_t K, int64_t L, bool al) {
     if (K == 128 && L == 128) return fast<kFused, 32, 1, 4, 4, kFS, kPU128>();
     if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, kFS, kPU>();
     if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, kFS, 16>();
+    switch (K) {
+      case 16: return fused_fast_l<16>(L);
+      case 32: return fused_fast_l<32>(L);
+      case 64: return fused_fast_l<64>(L);
+      case 128: return fused_fast_l<128>(L);
+      case 256: return fused_fast_l<256>(L);
+      case 512: return fused_fast_l<512>(L);
+      default: break;
+    }
   }
   return generic<kFused>();
 }
@@ -226,6 +293,7 @@ Variant pick_sddmm(int64_t K, bool al) {
     if (K == 64) return fast<kSddmm, 16, 1, 4, 4, kUS, kPU>();
     if (K == 128) return fast<kSddmm, 32, 1, 4, 4, kUS, kPU128>();
     if (K == 256) return fast<kSddmm, 64, 1, 4, 4, kUS, kPU>();
+    if (K == 512) return fast<kSddmm, 64, 1, 8, 4, kUS, kPU>();
   }
   return generic<kSddmm>();
 }

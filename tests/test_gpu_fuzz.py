@@ -49,10 +49,11 @@ def dev(a):
 
 
 FUSED_WIDTHS = [(32, 32), (64, 64), (128, 128), (256, 256), (16, 256), (16, 16), (3, 7),
-                (48, 80), (128, 64), (1, 300)]
+                (48, 80), (128, 64), (1, 300), (32, 128), (64, 16), (16, 512), (512, 128),
+                (128, 512), (256, 64)]
 
 
-@pytest.mark.parametrize("seed", range(20))
+@pytest.mark.parametrize("seed", range(32))
 def test_fuzz_fused_and_unfused(gpu, seed):
     rng = np.random.default_rng(1000 + seed)
     K, L = FUSED_WIDTHS[seed % len(FUSED_WIDTHS)]

@@ -89,6 +89,25 @@ def test_one_dense_row(gpu, K, L):
     check_A_rows(p, Au)
 
 
+WIDTHS = [16, 32, 64, 128, 256, 512]
+
+
+@pytest.mark.parametrize("K", WIDTHS)
+@pytest.mark.parametrize("L", WIDTHS)
+def test_fused_every_width_pair(gpu, K, L):
+    # every K, L pair of the fast variants (and the few that fall back to the
+    # generic kernel): power-law rows, one 9000-nonzero row split over many
+    # workers, 30% empty rows
+    n = power_law_lengths(2300, seed=K * 7 + L, cap=2000)
+    n[11] = 9000
+    p = make_problem(n, 2500, K, L, seed=K + 3 * L, dense="normal")
+    d = upload(p)
+    check_A_rows(p, fused(d))
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au)
+
+
 @pytest.mark.parametrize("L", [16, 32, 512, 12])
 def test_one_dense_row_spmm_widths(gpu, L):
     # the SpMM alone on one row split over every worker, at the narrowest and
