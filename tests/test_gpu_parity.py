@@ -108,6 +108,43 @@ def test_fused_every_width_pair(gpu, K, L):
     check_A_rows(p, Au)
 
 
+def _large_problem(N, K, L, seed):
+    """Enough rows for several resident grids (the wide-worker kernels): Pareto
+    row lengths with 30% empty rows and one 20000-nonzero row, built without a
+    per-row loop; columns sorted within rows, repeats allowed."""
+    rng = np.random.default_rng(seed)
+    lengths = power_law_lengths(N, seed=seed, scale=2.0, cap=3000)
+    lengths[N // 3] = 20_000
+    rowptr = np.zeros(N + 1, np.int64)
+    rowptr[1:] = np.cumsum(lengths)
+    nnz = int(rowptr[-1])
+    rows = np.repeat(np.arange(N), lengths)
+    cols = rng.integers(0, N, size=nnz)
+    order = np.lexsort((cols, rows))
+    colidx = cols[order].astype(np.int32)
+    vals = synth.uniform(seed, synth.STREAM_VALS, nnz, -1.0, 1.0)
+    C = synth.normal(seed, synth.STREAM_C, (N, K))
+    D = synth.normal(seed, synth.STREAM_D, (N, K))
+    E = synth.normal(seed, synth.STREAM_E, (N, L))
+    return synth.Problem("large", N, N, K, L, rowptr.astype(np.int32), colidx, vals, C, D, E)
+
+
+@pytest.mark.parametrize("K,L", [(64, 64), (128, 128)])
+def test_large_input_wide_workers(gpu, K, L):
+    # 300000 rows need several resident grids at these widths, so the fused
+    # kernel and both unfused passes run with one 64-lane worker per wave;
+    # every row and every SDDMM value is checked, and a second call must give
+    # the same bits
+    p = _large_problem(300_000, K, L, seed=K)
+    d = upload(p)
+    A = fused(d)
+    check_A_rows(p, A, what="fused A")
+    assert bool((fused(d) == A).all()), "fused result not deterministic"
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au, what="unfused A")
+
+
 @pytest.mark.parametrize("L", [16, 32, 512, 12])
 def test_one_dense_row_spmm_widths(gpu, L):
     # the SpMM alone on one row split over every worker, at the narrowest and
