@@ -113,9 +113,18 @@ __device__ __forceinline__ float bperm_f(int src_lane, float v) {
       float, __builtin_amdgcn_ds_bpermute(src_lane << 2, __builtin_bit_cast(int, v)));
 }
 
+__device__ __forceinline__ float readlane(float v, int lane) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
 // Sum over aligned groups of G lanes; every lane of the group receives the
 // same bits (each step adds a value and its partner's, and fp addition is
-// commutative).
+// commutative).  Inside rows of 16 lanes the steps are DPP moves; the rows
+// of a 32- or 64-lane group are then combined from their first lanes read
+// into scalar registers, (R0 + R1) + (R2 + R3), the same sums as an
+// exchange of halves would form, without a trip through the LDS unit.  The
+// callers keep each group's lanes active together, so the lanes read hold
+// the group's own row sums.
 template <int G>
 __device__ __forceinline__ float group_sum(float v) {
   static_assert(G == 1 || G == 2 || G == 4 || G == 8 || G == 16 || G == 32 || G == 64,
@@ -124,9 +133,13 @@ __device__ __forceinline__ float group_sum(float v) {
   if constexpr (G >= 4) v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]: lane ^ 2
   if constexpr (G >= 8) v += dpp<0x141>(v);  // row_half_mirror: other quad of 8
   if constexpr (G >= 16) v += dpp<0x140>(v); // row_mirror: other half of 16
-  if constexpr (G >= 32)                     // swizzle bit mode, xor 16
-    v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
-  if constexpr (G >= 64) v += bperm_f((int)(threadIdx.x & 63) ^ 32, v);
+  if constexpr (G == 32) {
+    const float lo = readlane(v, 0) + readlane(v, 16);
+    const float hi = readlane(v, 32) + readlane(v, 48);
+    return (threadIdx.x & 32) ? hi : lo;
+  }
+  if constexpr (G == 64)
+    return (readlane(v, 0) + readlane(v, 16)) + (readlane(v, 32) + readlane(v, 48));
   return v;
 }
 
