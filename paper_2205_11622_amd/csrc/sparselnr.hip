@@ -198,6 +198,11 @@ constexpr int kPU128 = SLNR_PACED_U128;
 #endif
 constexpr int kPUs = SLNR_PACED_U_SMALL;
 
+// The 64-lane fused kernel of large inputs at K = L = 128 takes 10 nonzeros
+// per paced step (measured on MI355X, R-MAT 2^20: 1.5-2.3% faster than 8 on
+// two boxes; 6 and 16 slower, as are 2 or 3 loads in flight per issue).
+constexpr int kPU128W = 10;
+
 Variant with_small(Variant v, KernelFn small) {
   v.fn_small = small;
   return v;
@@ -288,7 +293,7 @@ Variant pick_fused(int64_t K, int64_t L, bool al) {
       return with_wide<kFused, 1, 1, kFS, kPU>(with_small(
           fast<kFused, 16, 1, 4, 4, kFS, kPU>(), slnr::walk_fast<kFused, 16, 1, 4, 4, kFS, kPUs>));
     if (K == 128 && L == 128)
-      return with_wide<kFused, 2, 2, kFS, kPU128>(fast<kFused, 32, 1, 4, 4, kFS, kPU128>());
+      return with_wide<kFused, 2, 2, kFS, kPU128W>(fast<kFused, 32, 1, 4, 4, kFS, kPU128>());
     if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, kFS, kPU>();
     if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, kFS, 16>();
     switch (K) {
