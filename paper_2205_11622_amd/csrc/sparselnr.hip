@@ -172,7 +172,8 @@ Variant generic() {
 // Gather schedule of the fused kernels and of the unfused (SDDMM, SpMM)
 // kernels, each set to what measured fastest for it on MI355X: the fused
 // kernels pace their gathers, the unfused ones pipeline them.  Nonzeros per
-// step of the paced schedule: 8 for the 128-wide rows, 4 otherwise.
+// step of the paced schedule: 8 for the 128-wide rows, 4 otherwise (the
+// 64-lane kernels of large inputs take their own, below).
 #ifndef SLNR_FUSED_SCHED
 #define SLNR_FUSED_SCHED 1
 #endif
