@@ -145,6 +145,27 @@ def test_large_input_wide_workers(gpu, K, L):
     check_A_rows(p, Au, what="unfused A")
 
 
+@pytest.mark.parametrize("K,L", [(64, 64), (128, 128)])
+def test_large_input_wide_workers_unsorted(gpu, K, L):
+    # the wide kernels on columns that are neither sorted nor distinct within
+    # rows (duplicates add), and the SpMM entry point on its own; all rows
+    # of a 320000-row input (above the large-input size at every kernel's
+    # occupancy) are checked
+    rng = np.random.default_rng(K + 1)
+    p = _large_problem(320_000, K, L, seed=K + 7)
+    for i in rng.choice(p.N, size=3000, replace=False):  # shuffle some rows' columns
+        a, b = int(p.rowptr[i]), int(p.rowptr[i + 1])
+        if b - a > 1:
+            p.colidx[a:b] = rng.permutation(p.colidx[a:b])
+    d = upload(p)
+    check_A_rows(p, fused(d), what="fused A")
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au, what="unfused A")
+    A2 = slnr.sparselnr_spmm(d["rowptr"], d["colidx"], Y, d["E"])
+    assert bool((A2 == Au).all()), "sparselnr_spmm differs from the SpMM pass of the unfused call"
+
+
 @pytest.mark.parametrize("L", [16, 32, 512, 12])
 def test_one_dense_row_spmm_widths(gpu, L):
     # the SpMM alone on one row split over every worker, at the narrowest and
