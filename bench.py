@@ -4,7 +4,10 @@
     python bench.py [--steps K] [--warmup W] [--config rmat1m] [--kernel sddmm_spmm]
 
 One step is one library call over the whole matrix (merge-path walk kernel +
-carry fixup kernel), inputs resident in HBM.  The default is
+carry fixup kernel), inputs resident in HBM.  Before the timed region the
+library's grid factor (resident grids per walk launch) is chosen per call:
+the timed call and each pass of the comparison run at the fastest of a fixed
+candidate list (--grid-factor / --compare-grid-factor fix them instead).  The default is
 sparselnr_fused_sddmm_spmm on the R-MAT graph with 2^20 vertices, 16 edges
 per vertex drawn (duplicates merged, 16,085,851 nonzeros), K = L = 128,
 seed 0.
@@ -49,6 +52,11 @@ KERNEL_SOURCES = ["paper_2205_11622_amd/csrc/walker.hpp", "paper_2205_11622_amd/
                   "paper_2205_11622_amd/csrc/sparselnr.hip"]
 KERNELS = ("sddmm_spmm", "sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt")
 CPU_SECONDS = 10.0  # oracle passes are repeated until about this much wall time
+# Grid factors (resident grids per walk launch) tried for each library call
+# before the timed region; the timed call and each pass of the comparison run
+# at their own fastest one.
+GRID_FACTORS = (1, 2, 4, 8, 12, 16, 24, 32, 48, 64)
+TUNE_CALLS = 5
 
 
 def source_digest() -> str:
@@ -106,10 +114,13 @@ def make_workload(kernel, config, dev):
             "fused SDDMM→SpMM Gnnz/s + achieved HBM GB/s vs peak, %s K=%d L=%d" % (config, p.K, p.L),
             desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A, stream=stream),
-            compare=lambda: slnr.sparselnr_unfused_sddmm_spmm(rp, ci, v, C, D, E, Y, A2,
-                                                              stream=stream),
+            compare_parts=[
+                ("sparselnr_sddmm", lambda: slnr.sparselnr_sddmm(rp, ci, v, C, D, Y,
+                                                                 stream=stream)),
+                ("sparselnr_spmm", lambda: slnr.sparselnr_spmm(rp, ci, Y, E, A2,
+                                                               stream=stream))],
             compare_desc="library unfused path: sparselnr_sddmm into an nnz-sized Y, then "
-                         "sparselnr_spmm",
+                         "sparselnr_spmm, each pass at its own grid factor",
             bytes=p.model_bytes(), bytes_model="4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
             footprint=csr_bytes + 4 * (N * p.K + M * p.K + M * p.L + N * p.L),
             dominant="walk_fast fused + carry_fixup (one call)",
@@ -134,7 +145,7 @@ def make_workload(kernel, config, dev):
                    "%s K=L=M=64" % config, desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, C, D, F, W, A,
                                                               stream=stream),
-            compare=two_pass,
+            compare_parts=[("comparison", two_pass)],
             compare_desc="sparselnr_fused_sddmm_spmm into an N x L temporary, then torch.mm "
                          "by W",
             bytes=csr_bytes + 4 * nnz * (K + L) + 4 * N * K + 4 * N * Mo + 4 * L * Mo,
@@ -161,7 +172,7 @@ def make_workload(kernel, config, dev):
             metric="fused <SpMM,GEMM> Gnnz/s + achieved HBM GB/s vs peak, %s K=128 L=64"
                    % config, desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_spmm_gemm(rp, ci, v, C, D, A, stream=stream),
-            compare=two_pass,
+            compare_parts=[("comparison", two_pass)],
             compare_desc="sparselnr_spmm (B C) into an N x K temporary, then torch.mm by D",
             bytes=csr_bytes + 4 * nnz * K + 4 * K * L + 4 * N * L,
             bytes_model="4(N+1) + 8 nnz + 4 nnz K + 4 K L + 4 N L",
@@ -192,7 +203,7 @@ def make_workload(kernel, config, dev):
             metric="fused <SpMMH,GEMM> Gnnz/s + achieved HBM GB/s vs peak, %s J=L=128" % config,
             desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_spmmh_gemm(rp, ci, v, C, D, E, A, stream=stream),
-            compare=two_pass,
+            compare_parts=[("comparison", two_pass)],
             compare_desc="torch.mul C .* D into an M x J temporary, sparselnr_spmm into an "
                          "N x J temporary, then torch.mm by E",
             bytes=(12 * M * J + csr_bytes + 4 * nnz * J + 4 * J * L + 4 * N * L) if hoisted
@@ -218,8 +229,9 @@ def make_workload(kernel, config, dev):
                    "%s K=L=%d" % (config, p.K), desc=desc, sizes=w,
             call=lambda: slnr.sparselnr_fused_sddmm_spmm_dt(rp, ci, v, C, Dt, E, A,
                                                             stream=stream),
-            compare=lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A2,
-                                                            stream=stream),
+            compare_parts=[("sparselnr_fused_sddmm_spmm",
+                            lambda: slnr.sparselnr_fused_sddmm_spmm(rp, ci, v, C, D, E, A2,
+                                                                    stream=stream))],
             compare_desc="sparselnr_fused_sddmm_spmm on D stored M x K (the cost of the layout)",
             bytes=p.model_bytes() + 8 * M * p.K,
             bytes_model="8 M K (transpose pass) + 4(N+1) + 8 nnz + 4 nnz (K+L) + 4 N K + 4 N L",
@@ -332,6 +344,13 @@ def main() -> int:
     ap.add_argument("--sweep", action="store_true",
                     help="with --kernel sddmm_spmm or spmm_gemm: the fused call against the "
                          "separate passes over K, L in {16..512} (one JSON line per point)")
+    ap.add_argument("--grid-factor", default="auto",
+                    help="resident grids per walk launch for the timed call: 'auto' (fastest "
+                         "of %s, chosen before the timed region) or a fixed value in 1..64"
+                         % ",".join(map(str, GRID_FACTORS)))
+    ap.add_argument("--compare-grid-factor", default="auto",
+                    help="the same for the comparison: 'auto', one value for every pass, or "
+                         "one comma-separated value per pass")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -388,21 +407,65 @@ def main() -> int:
                                                     time.time() - t0),
           file=sys.stderr, flush=True)
 
-    per, total_ms, wall = timed(wl["call"], args.steps, args.warmup)
+    import paper_2205_11622_amd as slnr
+    set_factor = slnr.lib().sparselnr_set_grid_factor
+
+    def tune(name, fn):
+        """Fastest grid factor for one library call: per candidate, one untimed
+        call, then the median of TUNE_CALLS timed ones."""
+        res = {}
+        for f in GRID_FACTORS:
+            slnr.sparselnr_set_grid_factor(f)
+            res[f] = round(float(np.median(timed(fn, TUNE_CALLS, 1)[0])), 5)
+        best = min(res, key=res.get)
+        print("# grid factor for %s: %d (%s)" % (name, best, " ".join(
+            "%d:%.4f" % kv for kv in res.items())), file=sys.stderr, flush=True)
+        return best, res
+
+    def factors_for(parts, spec, what):
+        if spec == "auto":
+            chosen = [tune(name, fn) for name, fn in parts]
+            return [c[0] for c in chosen], {name: c[1] for (name, _), c in zip(parts, chosen)}
+        vals = [int(x) for x in spec.split(",")]
+        if len(vals) == 1:
+            vals = vals * len(parts)
+        if len(vals) != len(parts) or not all(1 <= f <= 64 for f in vals):
+            raise SystemExit("%s: need 'auto' or %d value(s) in 1..64" % (what, len(parts)))
+        return vals, None
+
+    def bound(parts, factors):
+        calls = list(zip(factors, [fn for _, fn in parts]))
+
+        def run():
+            for f, fn in calls:
+                set_factor(f)
+                fn()
+        return run
+
+    call_parts = [("timed call", wl["call"])]
+    call_factors, call_tuning = factors_for(call_parts, args.grid_factor, "--grid-factor")
+    call = bound(call_parts, call_factors)
+    per, total_ms, wall = timed(call, args.steps, args.warmup)
     ms = total_ms / args.steps
     print("# fused: %.4f ms/call (median %.4f, min %.4f, max %.4f)"
           % (ms, np.median(per), per.min(), per.max()), file=sys.stderr, flush=True)
     unf = None
+    cmp_tuning = None
     if not args.no_unfused:
-        uper, utotal, _ = timed(wl["compare"], args.steps, args.warmup)
+        parts = wl["compare_parts"]
+        cmp_factors, cmp_tuning = factors_for(parts, args.compare_grid_factor,
+                                              "--compare-grid-factor")
+        uper, utotal, _ = timed(bound(parts, cmp_factors), args.steps, args.warmup)
         # interleave a second fused round so both see the same machine state
-        per2, total2, _ = timed(wl["call"], args.steps, 1)
+        per2, total2, _ = timed(call, args.steps, 1)
         unf = {"what": wl["compare_desc"], "ms_per_call": utotal / args.steps,
                "median_ms": float(np.median(uper)), "fused_ms_rerun": total2 / args.steps,
-               "fused_speedup": (utotal / args.steps) / ms}
+               "fused_speedup": (utotal / args.steps) / ms,
+               "grid_factors": {name: f for (name, _), f in zip(parts, cmp_factors)}}
         print("# comparison: %.4f ms/call; fused rerun %.4f ms" % (unf["ms_per_call"],
                                                                   unf["fused_ms_rerun"]),
               file=sys.stderr, flush=True)
+    slnr.sparselnr_set_grid_factor(0)
 
     # context for comparing runs across machines: the rate of torch's own
     # 1 GiB device-to-device copy (read + write = 2 GiB moved)
@@ -462,6 +525,13 @@ def main() -> int:
         "median_ms": round(float(np.median(per)), 5), "min_ms": round(float(per.min()), 5),
         "p90_ms": round(float(np.percentile(per, 90)), 5), "wall_s": round(wall, 3),
         "unfused": unf, "source_digest": source_digest(),
+        "launch": {"grid_factor": call_factors[0],
+                   "chosen_by": "'auto': fastest of %s, median of %d calls each, before the "
+                                "timed region; else fixed on the command line (timed call %s, "
+                                "comparison %s)" % (list(GRID_FACTORS), TUNE_CALLS,
+                                                    args.grid_factor, args.compare_grid_factor),
+                   "tuning_ms": {"timed call": call_tuning and call_tuning["timed call"],
+                                 "comparison": cmp_tuning}},
     }
     print(json.dumps(out), flush=True)
     return 0

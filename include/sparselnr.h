@@ -210,6 +210,29 @@ SPARSELNR_API const char *sparselnr_status_string(int status);
  * calling thread (0 if none). */
 SPARSELNR_API int sparselnr_last_hip_error(void);
 
+/*
+ * Launch tuning (no counterpart in the paper, which fixes no GPU launch).
+ * Every walk launch runs `factor` resident grids of workers, each worker
+ * taking one merge-path slice of rows + nonzeros, so a larger factor gives
+ * more, shorter slices: the workers resident at one moment then cover a
+ * narrower band of rows, which changes how D and E rows are shared in the
+ * caches.  factor 0 restores the automatic choice (8 when the matrix has at
+ * least 8 rows per resident worker, else 1); 1..64 fixes the factor for every
+ * later call in the process, on every device and stream (the environment
+ * variable SPARSELNR_GRID_FACTOR gives the first value).  Results are
+ * deterministic for a fixed factor; another factor splits rows between slices
+ * elsewhere and so changes the fp32 summation order (within the accuracy
+ * stated for each entry point).  The carry workspace grows with the number
+ * of workers: 2 * L floats per worker.  Launches already made are not
+ * affected.  Returns SPARSELNR_OK, or SPARSELNR_ERR_INVALID_ARG for a factor
+ * outside 0..64.
+ */
+SPARSELNR_API int sparselnr_set_grid_factor(int factor);
+
+/* The factor fixed by sparselnr_set_grid_factor or SPARSELNR_GRID_FACTOR,
+ * or 0 when it is chosen per call. */
+SPARSELNR_API int sparselnr_get_grid_factor(void);
+
 /* Waits for the device(s) and frees every workspace the library allocated.
  * Safe to call at any time; later calls allocate again. */
 SPARSELNR_API int sparselnr_release(void);

@@ -25,7 +25,8 @@ __all__ = [
     "sparselnr_fused_sddmm_spmm", "sparselnr_unfused_sddmm_spmm", "sparselnr_sddmm",
     "sparselnr_spmm", "sparselnr_fused_sddmm_spmm_gemm", "sparselnr_spmm_gemm",
     "sparselnr_spmmh_gemm", "sparselnr_fused_sddmm_spmm_dt", "sparselnr_validate_csr", "sparselnr_release", "sparselnr_status_string",
-    "sparselnr_last_hip_error", "sparselnr_abi_version", "SparseLNRError", "lib", "LIB_PATH",
+    "sparselnr_last_hip_error", "sparselnr_abi_version", "sparselnr_set_grid_factor",
+    "sparselnr_get_grid_factor", "SparseLNRError", "lib", "LIB_PATH",
 ]
 
 
@@ -76,6 +77,10 @@ def lib() -> ctypes.CDLL:
         L.sparselnr_release.restype = ci
         L.sparselnr_abi_version.argtypes = []
         L.sparselnr_abi_version.restype = ci
+        L.sparselnr_set_grid_factor.argtypes = [ci]
+        L.sparselnr_set_grid_factor.restype = ci
+        L.sparselnr_get_grid_factor.argtypes = []
+        L.sparselnr_get_grid_factor.restype = ci
         _lib = L
     return _lib
 
@@ -90,6 +95,17 @@ def sparselnr_status_string(status: int) -> str:
 
 def sparselnr_last_hip_error() -> int:
     return int(lib().sparselnr_last_hip_error())
+
+
+def sparselnr_set_grid_factor(factor: int) -> None:
+    """Resident grids per walk launch: 0 automatic, 1..64 fixed (process-wide)."""
+    rc = lib().sparselnr_set_grid_factor(int(factor))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_set_grid_factor")
+
+
+def sparselnr_get_grid_factor() -> int:
+    return int(lib().sparselnr_get_grid_factor())
 
 
 def sparselnr_release() -> None:

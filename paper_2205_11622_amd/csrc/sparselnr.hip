@@ -3,6 +3,7 @@
 // include/sparselnr.h.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <cstdlib>
 #include <map>
@@ -56,7 +57,11 @@ struct Workspace {
 std::mutex g_mu;
 std::map<int, int> g_cus;                                    // device -> CUs
 std::map<std::pair<int, uintptr_t>, int> g_occupancy;        // (device, kernel) -> blocks/CU
-int g_grid_factor = 0;  // resident grids per launch (SPARSELNR_GRID_FACTOR; -1: by size)
+// Resident grids per walk launch: 0 not read yet (SPARSELNR_GRID_FACTOR gives
+// the first value), -1 chosen per call by size, 1..kMaxGridFactor fixed
+// (sparselnr_set_grid_factor).
+constexpr int kMaxGridFactor = 64;
+std::atomic<int> g_grid_factor{0};
 // workspaces per (device, stream, slot): slot 0 carry partials, slot 1 the
 // transposed D of the transposed-D entry point
 struct WsKey {
@@ -141,6 +146,8 @@ struct Variant {
   KernelFn fn_small = nullptr;  // same mapping, for inputs that fit one resident grid
   KernelFn fn_wide = nullptr;   // wider workers, for inputs that need several resident grids
   int W_wide = 64;
+  KernelFn fn_fine = nullptr;   // same mapping, for grids of at least fine_factor resident grids
+  int fine_factor = 0;
 };
 
 template <int MODE, int W, int NB, int KV, int LV, int SCHED = slnr::kPipelined, int U = 1>
@@ -230,6 +237,25 @@ Variant with_wide(Variant v) {
   return v;
 }
 
+// Fine slices (many resident grids per launch) take the pipelined schedule.
+// Measured on MI355X, the fused kernel at K = 16, L = 256 on the 27-point
+// stencil of a 128^3 grid (2^21 rows), ms per call by resident grids:
+//             8     12     24     48     64
+//   paced   5.85  5.77   5.79   5.80   6.02
+//   piped   6.61  6.10   5.61   5.04   5.09
+// With fine slices the rows walked at one moment on an XCD lie close
+// together and their E rows come back from the caches; the pipelined walk
+// holds 56 fewer registers of gathered rows than the 16-nonzero paced step,
+// so more waves share the CU and more gathers are in flight.  With coarse
+// slices the gathers go further out and the paced walk, which keeps fewer
+// in flight per wave, is faster.
+template <int MODE, int W, int NB, int KV, int LV, int U>
+Variant with_fine(Variant v, int from) {
+  v.fn_fine = slnr::walk_fast<MODE, W, NB, KV, LV, slnr::kPipelined, U>;
+  v.fine_factor = from;
+  return v;
+}
+
 // Lane mapping of a fused fast variant for K, L in {16, ..., 512}: the
 // consumer spreads E_j / A_i over W lanes of LV floats (L = W * LV); the
 // producer forms NB dot products per pass, each over PS = W / NB lanes of KV
@@ -303,7 +329,8 @@ Variant pick_fused(int64_t K, int64_t L, bool al) {
     if (K == 128 && L == 128)
       return with_wide<kFused, 2, 2, kFS, kPU128W>(fast<kFused, 32, 1, 4, 4, kFS, kPU128>());
     if (K == 256 && L == 256) return fast<kFused, 64, 1, 4, 4, kFS, kPU>();
-    if (K == 16 && L == 256) return fast<kFused, 64, 16, 4, 4, kFS, 16>();
+    if (K == 16 && L == 256)
+      return with_fine<kFused, 64, 16, 4, 4, 16>(fast<kFused, 64, 16, 4, 4, kFS, 16>(), 24);
     switch (K) {
       case 16: return fused_fast_l<16>(L);
       case 32: return fused_fast_l<32>(L);
@@ -371,10 +398,11 @@ struct Grid {
 // Resident blocks per CU for `fn` (occupancy query, cached per device).
 int blocks_per_cu(int dev, KernelFn fn, int block, size_t lds, int *out) {
   std::lock_guard<std::mutex> lock(g_mu);
-  if (g_grid_factor == 0) {
+  if (g_grid_factor.load() == 0) {
     const char *env = getenv("SPARSELNR_GRID_FACTOR");
     const int f = env ? atoi(env) : -1;
-    g_grid_factor = f >= 1 && f <= 64 ? f : -1;  // -1: chosen per call
+    int unset = 0;
+    g_grid_factor.compare_exchange_strong(unset, f >= 1 && f <= kMaxGridFactor ? f : -1);
   }
   auto key = std::make_pair(dev, (uintptr_t)fn);
   auto it = g_occupancy.find(key);
@@ -403,7 +431,7 @@ Grid make_grid(int cus, int per_cu, int block, int W, int64_t N, int factor = 0)
   Grid g;
   const int64_t resident_blocks = (int64_t)cus * per_cu;
   const int64_t resident_workers = resident_blocks * (block / 64) * (64 / W);
-  if (factor < 1) factor = g_grid_factor;
+  if (factor < 1) factor = g_grid_factor.load();
   if (factor < 1) factor = N >= 8 * resident_workers ? kGridFactor : 1;
   int blocks = (int)(resident_blocks * factor);
   blocks = ((blocks + kXcds - 1) / kXcds) * kXcds;
@@ -461,6 +489,10 @@ int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream
   } else if (nv == 1 && g.factor > 1 && v.fn_wide) {  // several grids: the wide workers
     v.fn = v.fn_wide;
     v.W = v.W_wide;
+    if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
+    g = make_grid(cus, per_cu, v.block, v.W, a.N, g.factor);
+  } else if (nv == 1 && v.fn_fine && g.factor >= v.fine_factor) {  // fine slices
+    v.fn = v.fn_fine;
     if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
     g = make_grid(cus, per_cu, v.block, v.W, a.N, g.factor);
   }
@@ -581,6 +613,20 @@ const char *sparselnr_status_string(int status) {
 }
 
 int sparselnr_last_hip_error(void) { return g_last_hip_error; }
+
+int sparselnr_set_grid_factor(int factor) {
+  if (factor < 0 || factor > kMaxGridFactor) return SPARSELNR_ERR_INVALID_ARG;
+  g_grid_factor.store(factor == 0 ? -1 : factor);
+  return SPARSELNR_OK;
+}
+
+int sparselnr_get_grid_factor(void) {
+  const int f = g_grid_factor.load();
+  if (f != 0) return f > 0 ? f : 0;
+  const char *env = getenv("SPARSELNR_GRID_FACTOR");
+  const int e = env ? atoi(env) : 0;
+  return e >= 1 && e <= kMaxGridFactor ? e : 0;
+}
 
 int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
                                const float *vals, const float *C, const float *D,

@@ -237,7 +237,7 @@ __device__ __forceinline__ int64_t mp_search(const int32_t *rowptr, int64_t N, i
     if (x > hi) x = hi;
     const bool ok = (int64_t)rowptr[x] + x <= d;
     const uint64_t ball = __ballot(ok);
-    const uint64_t bits = G == 64 ? ball : (ball >> gbase) & ((1ull << G) - 1);
+    const uint64_t bits = G == 64 ? ball : (ball >> gbase) & ((1ull << (G & 63)) - 1);
     const int m = (~bits == 0) ? 64 : __builtin_ctzll(~bits);  // probes 0..m-1 hold
     const int64_t xm1 = lo + (int64_t)m * step;                 // probe m-1 (if m > 0)
     const int64_t xm = lo + (int64_t)(m + 1) * step;            // probe m (if m < G)

@@ -47,6 +47,24 @@ def test_version_and_status_strings():
     assert slnr.sparselnr_status_string(0) == "ok"
 
 
+def test_grid_factor_setter():
+    lib = slnr.lib()
+    before = slnr.sparselnr_get_grid_factor()
+    try:
+        for f in (1, 8, 48, 64):
+            slnr.sparselnr_set_grid_factor(f)
+            assert slnr.sparselnr_get_grid_factor() == f
+        slnr.sparselnr_set_grid_factor(0)
+        assert slnr.sparselnr_get_grid_factor() == 0
+        for bad in (-1, 65, 1 << 20):
+            assert lib.sparselnr_set_grid_factor(bad) == slnr.ERR_INVALID_ARG
+            assert slnr.sparselnr_get_grid_factor() == 0
+        with pytest.raises(slnr.SparseLNRError):
+            slnr.sparselnr_set_grid_factor(-3)
+    finally:
+        slnr.sparselnr_set_grid_factor(before)
+
+
 NULL = None
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails validation first
 

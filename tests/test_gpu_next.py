@@ -157,6 +157,33 @@ def test_next_deterministic(gpu):
     assert torch.equal(A1.view(torch.int32), A2.view(torch.int32))
 
 
+@pytest.mark.parametrize("factor", [1, 5, 64])
+def test_next_grid_factors(gpu, factor):
+    # every entry point here at grid factors the benchmark may choose
+    # (sparselnr_set_grid_factor), down to mostly empty slices at 64
+    p = make_problem(lengths(17), 2400, 64, 64, seed=17, dense="normal")
+    W = synth.normal(5, 3, (64, 32))
+    Dk = synth.normal(3, 3, (64, 40))
+    E3 = synth.normal(4, 3, (64, 48))
+    Dt = np.ascontiguousarray(p.D.T)
+    try:
+        slnr.sparselnr_set_grid_factor(factor)
+        A = slnr.sparselnr_fused_sddmm_spmm_gemm(*csr(p), dev(p.C), dev(p.D), dev(p.E), dev(W))
+        ref, scale, _ = oracle.sddmm_spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, W)
+        assert_rows_close(rows_of(A, None), ref, scale, what="sddmm_spmm_gemm")
+        A = slnr.sparselnr_spmm_gemm(*csr(p), dev(p.D), dev(Dk))
+        ref, scale, _ = oracle.spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, Dk)
+        assert_rows_close(rows_of(A, None), ref, scale, what="spmm_gemm")
+        A = slnr.sparselnr_spmmh_gemm(*csr(p), dev(p.D), dev(p.E), dev(E3))
+        ref, scale, _ = oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, p.E, E3)
+        assert_rows_close(rows_of(A, None), ref, scale, what="spmmh_gemm")
+        A = slnr.sparselnr_fused_sddmm_spmm_dt(*csr(p), dev(p.C), dev(Dt), dev(p.E))
+        ref, scale, _ = oracle.fused_rows_dt(p.rowptr, p.colidx, p.vals, p.C, Dt, p.E)
+        assert_rows_close(rows_of(A, None), ref, scale, what="fused, D transposed")
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("kernel", ["sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt"])
 def test_next_on_rmat1m(gpu, kernel):

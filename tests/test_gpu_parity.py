@@ -166,6 +166,36 @@ def test_large_input_wide_workers_unsorted(gpu, K, L):
     assert bool((A2 == Au).all()), "sparselnr_spmm differs from the SpMM pass of the unfused call"
 
 
+@pytest.mark.parametrize("K,L", [(128, 128), (16, 256)])
+def test_grid_factors(gpu, K, L):
+    # every grid factor the benchmark may choose (sparselnr_set_grid_factor):
+    # each gives a correct, deterministic result; the SDDMM values do not
+    # depend on it among the factors that launch the same kernel; 0 restores
+    # the automatic choice
+    p = _large_problem(120_000, K, L, seed=7 + K)
+    d = upload(p)
+    rows = sample_rows(p, n_random=3000)
+    Y_wide = None
+    try:
+        for f in (1, 2, 3, 12, 48, 64):
+            slnr.sparselnr_set_grid_factor(f)
+            assert slnr.sparselnr_get_grid_factor() == f
+            A = fused(d)
+            check_A_rows(p, A, rows=rows, what="fused A, grid factor %d" % f)
+            assert bool((fused(d) == A).all()), "fused not deterministic at factor %d" % f
+            Y, Au = unfused(d)
+            check_Y(p, Y, rows=rows)
+            check_A_rows(p, Au, rows=rows, what="unfused A, grid factor %d" % f)
+            if f >= 2:
+                if Y_wide is None:
+                    Y_wide = Y
+                assert bool((Y == Y_wide).all()), "SDDMM values depend on the grid factor"
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
+    assert slnr.sparselnr_get_grid_factor() == 0
+    check_A_rows(p, fused(d), rows=rows, what="fused A, automatic grid factor")
+
+
 @pytest.mark.parametrize("L", [16, 32, 512, 12])
 def test_one_dense_row_spmm_widths(gpu, L):
     # the SpMM alone on one row split over every worker, at the narrowest and
