@@ -196,6 +196,28 @@ def test_grid_factors(gpu, K, L):
     check_A_rows(p, fused(d), rows=rows, what="fused A, automatic grid factor")
 
 
+@pytest.mark.slow
+def test_gathered_array_above_4gib(gpu):
+    # E holds M x 256 floats with M * 256 * 4 > 2^32 bytes: the gathers need
+    # 64-bit offsets, so every entry point takes the generic kernel.  Columns
+    # reach the last rows of E, and one row is split over many workers.
+    K, L = 16, 256
+    M = (1 << 32) // (4 * L) + 4096
+    lengths = power_law_lengths(3000, seed=11, scale=3.0, cap=2000)
+    lengths[1500] = 30_000
+    p = make_problem(lengths, M, K, L, seed=11, dups=True)
+    col = p.colidx.copy()
+    col[::7] = M - 1 - (np.arange(col[::7].size) % 4096)   # the rows past 4 GiB
+    p = synth.Problem("above 4 GiB", p.N, M, K, L, p.rowptr, col.astype(np.int32), p.vals,
+                      p.C, p.D, p.E)
+    assert M * L * 4 >= 1 << 32 and int(col.max()) == M - 1
+    d = upload(p)
+    check_A_rows(p, fused(d), what="fused A, E above 4 GiB")
+    Y, Au = unfused(d)
+    check_Y(p, Y)
+    check_A_rows(p, Au, what="unfused A, E above 4 GiB")
+
+
 @pytest.mark.parametrize("L", [16, 32, 512, 12])
 def test_one_dense_row_spmm_widths(gpu, L):
     # the SpMM alone on one row split over every worker, at the narrowest and
