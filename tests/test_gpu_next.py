@@ -188,34 +188,48 @@ def test_next_grid_factors(gpu, factor):
 @pytest.mark.parametrize("kernel", ["sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt"])
 def test_next_on_rmat1m(gpu, kernel):
     """The R-MAT 2^20 structure at the inner sizes the paper uses for each
-    benchmark (K=L=M=64; K=128, L=64; J=L=128), sampled rows."""
+    benchmark (K=L=M=64; K=128, L=64; J=L=128), sampled rows, at every grid
+    factor the benchmark may time and at the automatic one."""
     import torch
+
+    import bench
     base = synth.config("rmat1m")
     rows = sample_rows(base, n_random=1500)
     rp, ci, v = csr(base)
     if kernel == "sddmm_spmm_gemm":
         C, D, F = (synth.normal(0, s, (base.N, 64)) for s in (3, 4, 5))
         W = synth.normal(0, 6, (64, 64))
-        A = slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, dev(C), dev(D), dev(F), dev(W))
+        args = (rp, ci, v, dev(C), dev(D), dev(F), dev(W))
+        call = slnr.sparselnr_fused_sddmm_spmm_gemm
         ref, scale, _ = oracle.sddmm_spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, F,
                                                     W, rows=rows)
     elif kernel == "spmm_gemm":
         C, Dk = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 6, (128, 64))
-        A = slnr.sparselnr_spmm_gemm(rp, ci, v, dev(C), dev(Dk))
+        args = (rp, ci, v, dev(C), dev(Dk))
+        call = slnr.sparselnr_spmm_gemm
         ref, scale, _ = oracle.spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, Dk,
                                               rows=rows)
     elif kernel == "spmmh_gemm":
         C, D = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 5, (base.N, 128))
         E = synth.normal(0, 6, (128, 128))
-        A = slnr.sparselnr_spmmh_gemm(rp, ci, v, dev(C), dev(D), dev(E))
+        args = (rp, ci, v, dev(C), dev(D), dev(E))
+        call = slnr.sparselnr_spmmh_gemm
         ref, scale, _ = oracle.spmmh_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, E,
                                                rows=rows)
     else:
         Dt = np.ascontiguousarray(base.D.T)
-        A = slnr.sparselnr_fused_sddmm_spmm_dt(rp, ci, v, dev(base.C), dev(Dt), dev(base.E))
+        args = (rp, ci, v, dev(base.C), dev(Dt), dev(base.E))
+        call = slnr.sparselnr_fused_sddmm_spmm_dt
         ref, scale, _ = oracle.fused_rows_dt(base.rowptr, base.colidx, base.vals, base.C, Dt,
                                              base.E, rows=rows)
-    assert_rows_close(rows_of(A, rows), ref, scale, what=kernel)
-    assert not bool(torch.isnan(A).any())
+    try:
+        for f in (0,) + tuple(bench.GRID_FACTORS):
+            slnr.sparselnr_set_grid_factor(f)
+            A = call(*args)
+            assert_rows_close(rows_of(A, rows), ref, scale,
+                              what="%s, grid factor %s" % (kernel, f or "automatic"))
+            assert not bool(torch.isnan(A).any())
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
     del A
     torch.cuda.empty_cache()

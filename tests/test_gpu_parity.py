@@ -13,6 +13,7 @@ import paper_2205_11622_amd as slnr
 import synth
 from tests.gpu_util import (check_A_rows, check_Y, fused, make_problem, power_law_lengths,
                             sample_rows, unfused, upload)
+from tests.parity import assert_rows_close
 
 pytestmark = pytest.mark.gpu
 
@@ -228,7 +229,6 @@ def test_one_dense_row_spmm_widths(gpu, L):
     Y = torch.from_numpy(np.ascontiguousarray(p.vals)).to(gpu)
     A = slnr.sparselnr_spmm(d["rowptr"], d["colidx"], Y, d["E"])
     ref, scale, _ = oracle.spmm(p.rowptr, p.colidx, p.vals, p.E, Yabs=np.abs(p.vals))
-    from tests.parity import assert_rows_close
     assert_rows_close(A.cpu().numpy(), ref, scale)
 
 
@@ -310,7 +310,6 @@ def test_column_order_within_rows(gpu):
                       p.C, p.D, p.E)
     A2 = fused(upload(q)).cpu().numpy()
     ref, scale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E)
-    from tests.parity import assert_rows_close
     assert_rows_close(A2, A, 2 * scale)
 
 
@@ -364,14 +363,31 @@ def test_config_full(gpu, name):
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["rmat1m", "rmat4m", "banded"])
 def test_config_sampled(gpu, name):
+    # full size, at every grid factor the benchmark may time (it picks one
+    # per call from bench.GRID_FACTORS), and at the automatic one
     import torch
+
+    import bench
     p = synth.config(name)
     d = upload(p)
     rows = sample_rows(p)
-    check_A_rows(p, fused(d), rows, what=name + " fused")
-    Y, Au = unfused(d)
-    check_Y(p, Y, rows[:500])
-    check_A_rows(p, Au, rows, what=name + " unfused")
+    yrows = rows[:500]
+    ref, scale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, rows=rows)
+    _, _, Yref, Yscale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E,
+                                              rows=yrows, with_y=True)
+    yidx = torch.from_numpy(np.concatenate(
+        [np.arange(p.rowptr[i], p.rowptr[i + 1]) for i in yrows])).to(gpu)
+    rsel = torch.from_numpy(rows).to(gpu)
+    try:
+        for f in (0,) + tuple(bench.GRID_FACTORS):
+            slnr.sparselnr_set_grid_factor(f)
+            what = "%s, grid factor %s" % (name, f or "automatic")
+            assert_rows_close(fused(d)[rsel].cpu().numpy(), ref, scale, what=what + ", fused")
+            Y, Au = unfused(d)
+            assert_rows_close(Y[yidx].cpu().numpy(), Yref, Yscale, what=what + ", Y")
+            assert_rows_close(Au[rsel].cpu().numpy(), ref, scale, what=what + ", unfused")
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
     # every row of A written: no NaN left from a NaN-filled output
     A = torch.full((p.N, p.L), float("nan"), device=gpu)
     slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"], A)
