@@ -51,6 +51,14 @@
  *     sparselnr_release().
  *     Calls on different streams use different workspaces; calls on one
  *     stream are ordered by the stream.
+ *   - HIP graph capture: once a stream's workspace is large enough (after
+ *     one uncaptured call of the same size, width and grid factor on that
+ *     stream), a call launches kernels only, with no allocation,
+ *     synchronisation or memset, and can be captured on that stream.  The
+ *     graph records the workspace address: while it may still be replayed,
+ *     do not call sparselnr_release() and make no call on that stream that
+ *     needs a larger workspace (more rows, a wider L, a larger grid factor),
+ *     since either frees the workspace.
  *   - Results are deterministic: the same inputs give bit-identical outputs
  *     on the same device model (no floating-point atomics).
  *   - No C++ exception crosses this interface.

@@ -378,6 +378,45 @@ def test_two_streams_in_flight(gpu):
         assert torch.equal(Ab[t], Ab_ref), "stream 2, call %d differs from the call alone" % t
 
 
+def test_hip_graph_capture_and_replay(gpu):
+    # once a call on a stream has sized that stream's workspace, the fused and
+    # unfused calls launch kernels only, so a HIP graph can capture them; each
+    # replay, with eager calls in between, must give the eager result exactly
+    import torch
+    lengths = power_law_lengths(3000, seed=31, cap=3000)
+    lengths[5] = 12_000
+    p = make_problem(lengths, 2000, 32, 32, seed=31, dups=True)
+    d = upload(p)
+    args = (d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"])
+    s = torch.cuda.Stream()
+    A = torch.empty((p.N, p.L), dtype=torch.float32, device=gpu)
+    A2 = torch.empty_like(A)
+    Y = torch.empty(p.nnz, dtype=torch.float32, device=gpu)
+    with torch.cuda.stream(s):  # warm-up: sizes the workspace of s
+        slnr.sparselnr_fused_sddmm_spmm(*args, A=A, stream=s)
+        slnr.sparselnr_unfused_sddmm_spmm(*args, Y=Y, A=A2, stream=s)
+    s.synchronize()
+    ref, ref2, Yref = A.clone(), A2.clone(), Y.clone()
+    check_A_rows(p, ref, what="eager fused")
+    check_A_rows(p, ref2, what="eager unfused")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        slnr.sparselnr_fused_sddmm_spmm(*args, A=A, stream=s)
+        slnr.sparselnr_unfused_sddmm_spmm(*args, Y=Y, A=A2, stream=s)
+    for t in range(4):
+        A.fill_(float("nan"))
+        A2.fill_(float("nan"))
+        Y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(A, ref), "replay %d: fused result differs from eager" % t
+        assert torch.equal(A2, ref2), "replay %d: unfused result differs from eager" % t
+        assert torch.equal(Y, Yref), "replay %d: SDDMM values differ from eager" % t
+        assert torch.equal(fused(d), ref), "eager call after replay %d differs" % t
+        torch.cuda.synchronize()
+
+
 # ------------------------------------------------- the five named workloads
 
 @pytest.mark.parametrize("name", ["tiny", "uniform"])
