@@ -359,11 +359,17 @@ struct RowWalk {
   int64_t wb;  // nonzero window: wj = colidx[wb + glane], wv = vals[wb + glane]
   int wj;
   float wv;
+  // multi-dot SDDMM passes: this lane's slice of the D row of the next
+  // pass's nonzero, gathered one pass ahead.  (In the fused walk the same
+  // prefetch, issued ahead of the pass's E rows, measured 0-48% slower on the
+  // 27-point stencil, so the fused passes gather their own D rows.)
+  float dnext[KV];
+  int64_t pnext;  // first nonzero of the pass dnext belongs to (never a p otherwise)
 
   __device__ __forceinline__ RowWalk(const WalkArgs &a, int64_t p1_, uint32_t strideE_)
       : colidx(a.colidx), vals(a.vals), Dm(a.D), Em(a.E), Gm(a.G2), out(a.out), p1(p1_),
         strideD((uint32_t)a.K * 4u), strideE(strideE_), wb(-((int64_t)1 << 40)), wj(0),
-        wv(0.f) {
+        wv(0.f), pnext(-((int64_t)1 << 40)) {
     const int lane = threadIdx.x & 63;
     glane = lane & (W - 1);
     gbase = lane - glane;
@@ -500,16 +506,43 @@ struct RowWalk {
             const int src = (gbase + off + sub) & 63;
             const uint32_t js = (uint32_t)bperm_i(src, wj);
             const float bs = bperm_f(src, wv);
-            float dr[KV];
-            float t = 0.f;
-            if (act) {
-              ldv_off<KV>(dr, Dm, js * strideD + offD);
+            if constexpr (MODE == kSddmm) {
+              // the D rows of this pass, unless the previous pass gathered them
+              if (p != pnext && act) ldv_off<KV>(dnext, Dm, js * strideD + offD);
+              float t = 0.f;
+              if (act) {
   #pragma unroll
-              for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[v], t);
+                for (int v = 0; v < KV; ++v) t = fmaf(c[v], dnext[v], t);
+              }
+              t = group_sum<PS>(t);
+              y = bs * t;
+              if (act && q == 0) out[p + sub] = y;
+              // Gather the next pass's D rows before this pass's loop
+              // overhead and store.  The next pass starts at p + n and takes
+              // at most NB nonzeros, none past the window or the slice (it
+              // may belong to the next row: its dot waits for that row's C_i,
+              // not for D).  If the window ends here, the next pass refills
+              // it and gathers its own rows.
+              const int64_t pn = p + n;
+              const int offn = (int)(pn - wb) + sub;
+              const uint32_t jn = (uint32_t)bperm_i((gbase + offn) & 63, wj);
+              if (pn - wb < W) {
+                pnext = pn;
+                if (offn < W && pn + sub < p1) ldv_off<KV>(dnext, Dm, jn * strideD + offD);
+              } else {
+                pnext = -((int64_t)1 << 40);
+              }
+            } else {
+              float dr[KV];
+              float t = 0.f;
+              if (act) {
+                ldv_off<KV>(dr, Dm, js * strideD + offD);
+  #pragma unroll
+                for (int v = 0; v < KV; ++v) t = fmaf(c[v], dr[v], t);
+              }
+              t = group_sum<PS>(t);
+              y = bs * t;
             }
-            t = group_sum<PS>(t);
-            y = bs * t;
-            if (MODE == kSddmm && act && q == 0) out[p + sub] = y;
           }
           if (MODE != kSddmm && SCHED == kPaced) {
             // consumer: the whole worker streams each E row, one row issued
