@@ -4,8 +4,9 @@ Row counts from 1 to a few thousand (around the 64-lane window and the
 merge-path slice sizes), row-length mixes with empty rows, a single heavy
 row split over many workers, constant tiny rows, duplicate and unsorted
 columns, every width with a fast variant plus odd widths for the generic
-path, and any output width for the Section 6.2 products.  Same tolerance
-rule as tests/parity.py."""
+path, and any output width for the Section 6.2 products; the <SDDMM, SpMM>
+cases run again at a seeded grid factor.  Same tolerance rule as
+tests/parity.py."""
 import numpy as np
 import pytest
 
@@ -63,6 +64,16 @@ def test_fuzz_fused_and_unfused(gpu, seed):
     Y, Au = unfused(d)
     check_Y(p, Y)
     check_A_rows(p, Au, what="unfused seed %d" % seed)
+    # again at a fixed grid factor (sparselnr_set_grid_factor), drawn per seed
+    f = int(np.random.default_rng(5000 + seed).choice([1, 2, 3, 8, 24, 64]))
+    try:
+        slnr.sparselnr_set_grid_factor(f)
+        check_A_rows(p, fused(d), what="fused seed %d, grid factor %d" % (seed, f))
+        Y, Au = unfused(d)
+        check_Y(p, Y)
+        check_A_rows(p, Au, what="unfused seed %d, grid factor %d" % (seed, f))
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
 
 
 EPI_WIDTHS = [16, 32, 64, 128, 256, 512]
