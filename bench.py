@@ -351,6 +351,9 @@ def main() -> int:
     ap.add_argument("--compare-grid-factor", default="auto",
                     help="the same for the comparison: 'auto', one value for every pass, or "
                          "one comma-separated value per pass")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time each call after writing and reading a 1 GiB buffer (which evicts "
+                         "the 256 MB MALL and the L2s); reported as `cold`, never as `value`")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
@@ -465,6 +468,26 @@ def main() -> int:
         print("# comparison: %.4f ms/call; fused rerun %.4f ms" % (unf["ms_per_call"],
                                                                   unf["fused_ms_rerun"]),
               file=sys.stderr, flush=True)
+    cold = None
+    if args.cold:
+        flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        flush.fill_(0.0)
+        cper = []
+        ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for _ in range(args.steps):
+            flush.add_(1.0)  # reads and writes 1 GiB on the same stream, just before the call
+            ce[0].record(stream)
+            call()
+            ce[1].record(stream)
+            torch.cuda.synchronize()
+            cper.append(ce[0].elapsed_time(ce[1]))
+        del flush
+        torch.cuda.empty_cache()
+        cold = {"ms_per_call_median": round(float(np.median(cper)), 5),
+                "ms_per_call_min": round(float(np.min(cper)), 5), "calls": len(cper),
+                "flush": "1 GiB read and written on the stream before each call"}
+        print("# cold: %.4f ms/call (median)" % cold["ms_per_call_median"], file=sys.stderr,
+              flush=True)
     slnr.sparselnr_set_grid_factor(0)
 
     # context for comparing runs across machines: the rate of torch's own
@@ -524,7 +547,7 @@ def main() -> int:
         "footprint_bytes": wl["footprint"],
         "median_ms": round(float(np.median(per)), 5), "min_ms": round(float(per.min()), 5),
         "p90_ms": round(float(np.percentile(per, 90)), 5), "wall_s": round(wall, 3),
-        "unfused": unf, "source_digest": source_digest(),
+        "unfused": unf, "cold": cold, "source_digest": source_digest(),
         "launch": {"grid_factor": call_factors[0],
                    "chosen_by": "'auto': fastest of %s, median of %d calls each, before the "
                                 "timed region; else fixed on the command line (timed call %s, "
