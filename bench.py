@@ -57,6 +57,8 @@ CPU_SECONDS = 10.0  # oracle passes are repeated until about this much wall time
 # at their own fastest one.
 GRID_FACTORS = (1, 2, 4, 8, 12, 16, 24, 32, 48, 64)
 TUNE_CALLS = 5
+SMALL_CONFIGS = ("tiny", "uniform")  # calls of tens of microseconds: more timed calls by default
+SMALL_STEPS = 200
 
 
 def source_digest() -> str:
@@ -334,7 +336,9 @@ def sweep_sddmm_spmm(args, dev, timed) -> None:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed calls (default: 200 for the tiny and uniform workloads, whose calls "
+                         "take tens of microseconds, else 20)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="rmat1m")
     ap.add_argument("--kernel", default="sddmm_spmm", choices=KERNELS)
@@ -358,6 +362,8 @@ def main() -> int:
                     help="after timing, run three plain 1 GiB device copies (torch copy_), the "
                          "reference for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings")
     args = ap.parse_args()
+    if args.steps is None:
+        args.steps = SMALL_STEPS if args.config in SMALL_CONFIGS and not args.sweep else 20
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on exactly one GPU: the fused kernel shards by rows with no "
