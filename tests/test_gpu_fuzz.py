@@ -5,7 +5,7 @@ merge-path slice sizes), row-length mixes with empty rows, a single heavy
 row split over many workers, constant tiny rows, duplicate and unsorted
 columns, every width with a fast variant plus odd widths for the generic
 path, and any output width for the Section 6.2 products; the <SDDMM, SpMM>
-cases run again at a seeded grid factor.  Same tolerance rule as
+and Section 6.2 cases run again at a seeded grid factor.  Same tolerance rule as
 tests/parity.py."""
 import numpy as np
 import pytest
@@ -87,18 +87,28 @@ def test_fuzz_section62_products(gpu, seed):
     p = problem(rng, seed, lin, lin)
     rp, ci, v = dev(p.rowptr), dev(p.colidx), dev(p.vals)
     W = synth.normal(seed, 9, (lin, lout))
-    # <SDDMM, SpMM, GEMM>
-    A = slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, dev(p.C), dev(p.D), dev(p.E), dev(W))
-    ref, scale, _ = oracle.sddmm_spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, W)
-    assert_rows_close(A.cpu().numpy(), ref, scale, what="sddmm_spmm_gemm seed %d" % seed)
-    # <SpMM, GEMM> with C = D (M x lin)
-    A = slnr.sparselnr_spmm_gemm(rp, ci, v, dev(p.D), dev(W))
-    ref, scale, _ = oracle.spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, W)
-    assert_rows_close(A.cpu().numpy(), ref, scale, what="spmm_gemm seed %d" % seed)
-    # <SpMMH, GEMM> with C, D = D, E (M x lin each)
-    A = slnr.sparselnr_spmmh_gemm(rp, ci, v, dev(p.D), dev(p.E), dev(W))
-    ref, scale, _ = oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, p.E, W)
-    assert_rows_close(A.cpu().numpy(), ref, scale, what="spmmh_gemm seed %d" % seed)
+    refs = [oracle.sddmm_spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, W),
+            oracle.spmm_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, W),
+            oracle.spmmh_gemm_rows(p.rowptr, p.colidx, p.vals, p.D, p.E, W)]
+    # at the automatic grid factor, then at a seeded fixed one
+    f = int(np.random.default_rng(6000 + seed).choice([1, 2, 3, 8, 24, 64]))
+    try:
+        for factor in (0, f):
+            slnr.sparselnr_set_grid_factor(factor)
+            tag = "seed %d, grid factor %d" % (seed, factor)
+            # <SDDMM, SpMM, GEMM>
+            A = slnr.sparselnr_fused_sddmm_spmm_gemm(rp, ci, v, dev(p.C), dev(p.D), dev(p.E),
+                                                     dev(W))
+            assert_rows_close(A.cpu().numpy(), refs[0][0], refs[0][1],
+                              what="sddmm_spmm_gemm " + tag)
+            # <SpMM, GEMM> with C = D (M x lin)
+            A = slnr.sparselnr_spmm_gemm(rp, ci, v, dev(p.D), dev(W))
+            assert_rows_close(A.cpu().numpy(), refs[1][0], refs[1][1], what="spmm_gemm " + tag)
+            # <SpMMH, GEMM> with C, D = D, E (M x lin each)
+            A = slnr.sparselnr_spmmh_gemm(rp, ci, v, dev(p.D), dev(p.E), dev(W))
+            assert_rows_close(A.cpu().numpy(), refs[2][0], refs[2][1], what="spmmh_gemm " + tag)
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
 
 
 @pytest.mark.parametrize("seed", range(6))
