@@ -65,6 +65,26 @@ def test_grid_factor_setter():
         slnr.sparselnr_set_grid_factor(before)
 
 
+def test_grid_factor_environment():
+    # SPARSELNR_GRID_FACTOR gives the first value (1..64, anything else means
+    # automatic); sparselnr_set_grid_factor overrides it
+    import subprocess
+    import sys
+    code = ("import paper_2205_11622_amd as s; a = s.sparselnr_get_grid_factor(); "
+            "s.sparselnr_set_grid_factor(3); b = s.sparselnr_get_grid_factor(); "
+            "s.sparselnr_set_grid_factor(0); print(a, b, s.sparselnr_get_grid_factor())")
+    for env, want in (("12", "12 3 0"), ("64", "64 3 0"), ("65", "0 3 0"), ("0", "0 3 0"),
+                      ("x", "0 3 0"), (None, "0 3 0")):
+        e = dict(os.environ)
+        e.pop("SPARSELNR_GRID_FACTOR", None)
+        if env is not None:
+            e["SPARSELNR_GRID_FACTOR"] = env
+        r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                           timeout=120, cwd=ROOT, env=e)
+        assert r.returncode == 0, r.stderr
+        assert r.stdout.split() == want.split(), (env, r.stdout)
+
+
 NULL = None
 FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails validation first
 
