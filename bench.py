@@ -86,6 +86,14 @@ def stored_traffic(key: str):
     return t
 
 
+def device_info(dev) -> dict:
+    """The GPU the line was measured on (boxes of one model differ by up to 15%)."""
+    import torch
+    p = torch.cuda.get_device_properties(dev)
+    return {"name": p.name, "arch": getattr(p, "gcnArchName", ""), "cus": p.multi_processor_count,
+            "memory_GiB": round(p.total_memory / 2 ** 30, 1)}
+
+
 def make_workload(kernel, config, dev):
     """Inputs on the device, the timed call, the comparison call, the byte model
     and the oracle leg for one kernel."""
@@ -554,6 +562,7 @@ def main() -> int:
         "median_ms": round(float(np.median(per)), 5), "min_ms": round(float(per.min()), 5),
         "p90_ms": round(float(np.percentile(per, 90)), 5), "wall_s": round(wall, 3),
         "unfused": unf, "cold": cold, "source_digest": source_digest(),
+        "device": device_info(dev),
         "launch": {"grid_factor": call_factors[0],
                    "chosen_by": "'auto': fastest of %s, median of %d calls each, before the "
                                 "timed region; else fixed on the command line (timed call %s, "
