@@ -43,3 +43,4 @@ def test_bench_json_line(gpu):
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert d["unfused"]["ms_per_call"] > 0
     assert 1 <= d["launch"]["grid_factor"] <= 64
+    assert d["device"]["cus"] > 0 and "gfx950" in d["device"]["arch"]
