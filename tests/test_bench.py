@@ -14,7 +14,7 @@ def run(args, env=None):
     e = dict(os.environ)
     e.update(env or {})
     return subprocess.run([sys.executable, BENCH] + args, capture_output=True, text=True,
-                          timeout=120, cwd=ROOT, env=e)
+                          timeout=600, cwd=ROOT, env=e)
 
 
 def test_more_than_one_gpu_is_refused():
