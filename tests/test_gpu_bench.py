@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_bench_json_line(gpu):
     r = subprocess.run([sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--config", "tiny",
                         "--steps", "5", "--warmup", "1"],
-                       capture_output=True, text=True, timeout=240, cwd=ROOT)
+                       capture_output=True, text=True, timeout=480, cwd=ROOT)
     print(r.stderr[-2000:], flush=True)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [ln for ln in r.stdout.splitlines() if ln.strip()]
