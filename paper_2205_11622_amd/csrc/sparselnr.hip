@@ -185,7 +185,8 @@ Variant generic() {
 
 // Gather schedule of the fused kernels and of the unfused (SDDMM, SpMM)
 // kernels, each set to what measured fastest for it on MI355X: the fused
-// kernels pace their gathers, the unfused ones pipeline them.  Nonzeros per
+// kernels pace their gathers (the K = 16, L = 256 one only for coarse slices,
+// see with_fine), the unfused ones pipeline them.  Nonzeros per
 // step of the paced schedule: 8 for the 128-wide rows, 4 otherwise (the
 // 64-lane kernels of large inputs take their own, below).
 #ifndef SLNR_FUSED_SCHED

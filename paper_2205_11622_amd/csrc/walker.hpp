@@ -339,6 +339,17 @@ struct Gather {
 // divergence inside a wave only masks whole groups.  The colidx / vals window
 // (one entry per lane) keeps the dependent loads off the critical path; the
 // gathered D_j and E_j rows are plain loads so the hot columns stay in L2.
+// Gathers a paced step lets stay in flight when it issues its next nonzero:
+// one, except for the 64-lane worker with one float of each row per lane
+// (K = L = 64, large inputs), which takes two.  Measured on MI355X, R-MAT
+// 2^22: 1.5-2.3% faster than one at 16-64 resident grids, bit-identical;
+// three and no wait at all are within 0.5% of two.  The wider rows of rmat1m
+// and the stencil run slower with more than one.
+template <int W, int KV, int LV>
+constexpr int paced_in_flight() {
+  return W == 64 && KV == 1 && LV == 1 ? 2 : 1;
+}
+
 template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U, int HAD = 0>
 struct RowWalk {
   static constexpr int PS = W / NB;
@@ -361,8 +372,9 @@ struct RowWalk {
   float wv;
   // multi-dot SDDMM passes: this lane's slice of the D row of the next
   // pass's nonzero, gathered one pass ahead.  (In the fused walk the same
-  // prefetch, issued ahead of the pass's E rows, measured 0-48% slower on the
-  // 27-point stencil, so the fused passes gather their own D rows.)
+  // prefetch gains nothing at its best grid factor on the 27-point stencil,
+  // and its 8 extra registers cost a wave per SIMD, so the fused passes
+  // gather their own D rows.)
   float dnext[KV];
   int64_t pnext;  // first nonzero of the pass dnext belongs to (never a p otherwise)
 
@@ -413,7 +425,7 @@ struct RowWalk {
   #pragma unroll
           for (int u = 0; u < U; ++u) {
             if (u < n) {
-              if (u > 0) wait_vmcnt<1>();
+              if (u > 0) wait_vmcnt<paced_in_flight<W, KV, LV>()>();
               if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
               if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
               if constexpr (HAD) ldv_off<LV>(hr[u], Gm, jj[u] * strideE + offE);
