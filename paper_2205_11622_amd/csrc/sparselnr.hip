@@ -557,6 +557,20 @@ int check_range(int64_t N, int64_t M, int64_t K, int64_t L) {
   return SPARSELNR_OK;
 }
 
+// Argument checks of the fused <SDDMM, SpMM> entry points (plain and
+// transposed D): pointers, signs and ranges, all before any HIP call.
+int check_fused_args(const int32_t *rowptr, const int32_t *colidx, const float *vals,
+                     const float *C, const float *D, const float *E, const float *A, int64_t N,
+                     int64_t M, int64_t K, int64_t L) {
+  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && K > 0 && !C) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && K > 0 && !D) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
+  if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
+  return check_range(N, M, K, L);
+}
+
 WalkArgs base_args(const int32_t *rowptr, const int32_t *colidx, const float *vals,
                    int64_t N, int64_t K, int64_t L) {
   WalkArgs a{};
@@ -633,13 +647,7 @@ int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
                                const float *vals, const float *C, const float *D,
                                const float *E, float *A, int64_t N, int64_t M, int64_t K,
                                int64_t L, void *stream) {
-  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && (!rowptr || !colidx || !vals)) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && K > 0 && !C) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && M > 0 && K > 0 && !D) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
-  int rc = check_range(N, M, K, L);
+  int rc = check_fused_args(rowptr, colidx, vals, C, D, E, A, N, M, K, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
   const bool al = aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A) &&
@@ -793,9 +801,8 @@ int sparselnr_fused_sddmm_spmm_dt(const int32_t *rowptr, const int32_t *colidx,
                                   const float *vals, const float *C, const float *Dt,
                                   const float *E, float *A, int64_t N, int64_t M, int64_t K,
                                   int64_t L, void *stream) {
-  if (bad_size(N, M, K, L)) return SPARSELNR_ERR_INVALID_ARG;
-  if (N > 0 && M > 0 && K > 0 && !Dt) return SPARSELNR_ERR_INVALID_ARG;
-  int rc = check_range(N, M, K, L);
+  // every argument is checked before the transpose touches the device
+  int rc = check_fused_args(rowptr, colidx, vals, C, Dt, E, A, N, M, K, L);
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
   if (M == 0 || K == 0)  // D is empty: nothing to transpose

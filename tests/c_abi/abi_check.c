@@ -3,10 +3,20 @@
  * library).  It allocates device memory with the HIP C runtime API, calls
  * sparselnr_fused_sddmm_spmm and sparselnr_unfused_sddmm_spmm on a seeded
  * 1000-row matrix (row lengths 0..60 plus one 3000-nonzero row, K = L = 64),
- * and checks every row against the CPU oracle (oracle_fused_rows, linked
- * from oracle/liboracle.so) with the parity rule: per row,
- * max |A - Aref| <= 1e-4 * scale.  It also checks that argument errors come
- * back as status codes.  Prints "abi_check: ok" and exits 0 on success.
+ * and checks every row against the CPU oracle (oracle_fused_rows) with the
+ * parity rule: per row, max |A - Aref| <= 1e-4 * scale.  It also checks that
+ * argument errors come back as status codes.  Prints "abi_check: ok" and
+ * exits 0 on success.
+ *
+ * The program reports where it is: stdout is unbuffered, a marker goes to
+ * stderr before every phase, and an exit handler prints the last marker, so
+ * a crash anywhere (exit-time teardown included) leaves the phase it
+ * happened in.
+ *
+ * With --host-only it runs only the phases that need no GPU (input
+ * generation, the oracle, the comparison routine and the argument-error
+ * calls, which return before any HIP call) and exits; this is the mode the
+ * sanitizer build runs on a host without a GPU.
  */
 #define __HIP_PLATFORM_AMD__ 1
 #include <hip/hip_runtime_api.h>
@@ -14,6 +24,7 @@
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include "sparselnr.h"
 
@@ -22,6 +33,17 @@ int64_t oracle_fused_rows(int64_t N, int64_t M, int64_t K, int64_t L, const int3
                           const int32_t *colidx, const float *vals, const float *C,
                           const float *D, const float *E, const int64_t *rows, int64_t nrows,
                           double *A_out, double *scale_out, double *Y_out, double *Yscale_out);
+
+static const char *g_phase = "start";
+
+static void phase(const char *name) {
+  g_phase = name;
+  fprintf(stderr, "abi_check: phase %s\n", name);
+}
+
+static void at_exit_marker(void) {
+  fprintf(stderr, "abi_check: exit handlers reached (last phase: %s)\n", g_phase);
+}
 
 /* test-local input generator (64-bit LCG, top 24 bits -> [-1, 1)) */
 static uint64_t g_state = 12345;
@@ -65,8 +87,13 @@ static int compare(const char *what, const float *A, const double *ref, const do
   return 0;
 }
 
-int main(void) {
+int main(int argc, char **argv) {
+  setvbuf(stdout, NULL, _IONBF, 0);
+  atexit(at_exit_marker);
+  const int host_only = argc > 1 && strcmp(argv[1], "--host-only") == 0;
   const int64_t N = 1000, M = 800, K = 64, L = 64;
+
+  phase("inputs");
   int32_t *rowptr = malloc((N + 1) * sizeof(int32_t));
   rowptr[0] = 0;
   for (int64_t i = 0; i < N; ++i) {
@@ -87,6 +114,50 @@ int main(void) {
   for (int64_t t = 0; t < M * K; ++t) D[t] = next_f();
   for (int64_t t = 0; t < M * L; ++t) E[t] = next_f();
 
+  phase("oracle");
+  int64_t *rows = malloc(N * sizeof(int64_t));
+  for (int64_t i = 0; i < N; ++i) rows[i] = i;
+  double *ref = malloc(N * L * sizeof(double)), *scale = malloc(N * sizeof(double));
+  oracle_fused_rows(N, M, K, L, rowptr, colidx, vals, C, D, E, rows, N, ref, scale, NULL, NULL);
+
+  phase("compare routine on the oracle's own rows");
+  for (int64_t t = 0; t < N * L; ++t) A[t] = (float)ref[t];
+  if (compare("oracle rounded to fp32", A, ref, scale, N, L)) return 1;
+
+  /* argument errors are status codes, returned before any HIP call (the
+   * pointers below are never dereferenced) */
+  phase("argument errors");
+  void *fake = (void *)(uintptr_t)0x1000;
+  if (sparselnr_fused_sddmm_spmm(NULL, fake, fake, fake, fake, fake, fake, N, M, K, L, NULL) !=
+      SPARSELNR_ERR_INVALID_ARG) {
+    fprintf(stderr, "abi_check: NULL rowptr not rejected\n");
+    return 1;
+  }
+  if (sparselnr_fused_sddmm_spmm(fake, fake, fake, fake, fake, fake, fake, N, M, -1, L, NULL) !=
+      SPARSELNR_ERR_INVALID_ARG) {
+    fprintf(stderr, "abi_check: negative K not rejected\n");
+    return 1;
+  }
+  if (sparselnr_fused_sddmm_spmm_dt(fake, fake, fake, fake, fake, fake, NULL, N, M, K, L, NULL) !=
+      SPARSELNR_ERR_INVALID_ARG) {
+    fprintf(stderr, "abi_check: NULL A (transposed D) not rejected\n");
+    return 1;
+  }
+  if (sparselnr_unfused_sddmm_spmm(fake, fake, fake, fake, fake, fake, NULL, fake, N, M, K, L,
+                                   NULL) != SPARSELNR_ERR_INVALID_ARG) {
+    fprintf(stderr, "abi_check: NULL Y not rejected\n");
+    return 1;
+  }
+  if (host_only) {
+    phase("done (host only)");
+    printf("abi_check: host phases ok (N=%lld nnz=%lld K=%lld L=%lld)\n", (long long)N,
+           (long long)nnz, (long long)K, (long long)L);
+    free(rowptr); free(colidx); free(vals); free(C); free(D); free(E); free(A);
+    free(rows); free(ref); free(scale);
+    return 0;
+  }
+
+  phase("device setup");
   int dev_count = 0;
   if (hipGetDeviceCount(&dev_count) != hipSuccess || dev_count == 0) {
     fprintf(stderr, "abi_check: no GPU\n");
@@ -109,23 +180,8 @@ int main(void) {
   CHECK_HIP(hipMemcpy(d_D, D, M * K * sizeof(float), hipMemcpyHostToDevice));
   CHECK_HIP(hipMemcpy(d_E, E, M * L * sizeof(float), hipMemcpyHostToDevice));
 
-  /* argument errors are status codes, before any device work */
-  if (sparselnr_fused_sddmm_spmm(NULL, d_colidx, d_vals, d_C, d_D, d_E, d_A, N, M, K, L, NULL) !=
-      SPARSELNR_ERR_INVALID_ARG) {
-    fprintf(stderr, "abi_check: NULL rowptr not rejected\n");
-    return 1;
-  }
-  if (sparselnr_fused_sddmm_spmm(d_rowptr, d_colidx, d_vals, d_C, d_D, d_E, d_A, N, M, -1, L,
-                                 NULL) != SPARSELNR_ERR_INVALID_ARG) {
-    fprintf(stderr, "abi_check: negative K not rejected\n");
-    return 1;
-  }
-
-  int64_t *rows = malloc(N * sizeof(int64_t));
-  for (int64_t i = 0; i < N; ++i) rows[i] = i;
-  double *ref = malloc(N * L * sizeof(double)), *scale = malloc(N * sizeof(double));
-  oracle_fused_rows(N, M, K, L, rowptr, colidx, vals, C, D, E, rows, N, ref, scale, NULL, NULL);
-
+  phase("fused call");
+  CHECK_HIP(hipMemset(d_A, 0xff, N * L * sizeof(float))); /* NaN pattern: every row is written */
   int rc = sparselnr_fused_sddmm_spmm(d_rowptr, d_colidx, d_vals, d_C, d_D, d_E, d_A, N, M, K,
                                       L, NULL);
   if (rc != SPARSELNR_OK) {
@@ -136,7 +192,8 @@ int main(void) {
   CHECK_HIP(hipMemcpy(A, d_A, N * L * sizeof(float), hipMemcpyDeviceToHost));
   if (compare("fused", A, ref, scale, N, L)) return 1;
 
-  CHECK_HIP(hipMemset(d_A, 0xff, N * L * sizeof(float))); /* NaN pattern: every row is written */
+  phase("unfused call");
+  CHECK_HIP(hipMemset(d_A, 0xff, N * L * sizeof(float)));
   rc = sparselnr_unfused_sddmm_spmm(d_rowptr, d_colidx, d_vals, d_C, d_D, d_E, d_Y, d_A, N, M, K,
                                     L, NULL);
   if (rc != SPARSELNR_OK) {
@@ -147,9 +204,19 @@ int main(void) {
   CHECK_HIP(hipMemcpy(A, d_A, N * L * sizeof(float), hipMemcpyDeviceToHost));
   if (compare("unfused", A, ref, scale, N, L)) return 1;
 
+  phase("release and free");
   if (sparselnr_release() != SPARSELNR_OK) return 1;
-  hipFree(d_rowptr); hipFree(d_colidx); hipFree(d_vals); hipFree(d_C);
-  hipFree(d_D); hipFree(d_E); hipFree(d_A); hipFree(d_Y);
+  CHECK_HIP(hipFree(d_rowptr));
+  CHECK_HIP(hipFree(d_colidx));
+  CHECK_HIP(hipFree(d_vals));
+  CHECK_HIP(hipFree(d_C));
+  CHECK_HIP(hipFree(d_D));
+  CHECK_HIP(hipFree(d_E));
+  CHECK_HIP(hipFree(d_A));
+  CHECK_HIP(hipFree(d_Y));
+  free(rowptr); free(colidx); free(vals); free(C); free(D); free(E); free(A);
+  free(rows); free(ref); free(scale);
+  phase("return from main");
   printf("abi_check: ok (N=%lld nnz=%lld K=%lld L=%lld)\n", (long long)N, (long long)nnz,
          (long long)K, (long long)L);
   return 0;

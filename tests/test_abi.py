@@ -188,6 +188,35 @@ def test_next_entry_points_argument_errors():
     assert L.sparselnr_fused_sddmm_spmm_dt(*(FAKE,) * 7, -4, 4, 4, 4, NULL) == slnr.ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("entry", ["sparselnr_fused_sddmm_spmm", "sparselnr_fused_sddmm_spmm_dt"])
+@pytest.mark.parametrize("which", ["rowptr", "colidx", "vals", "C", "D", "E", "A"])
+def test_fused_null_pointer_rejected_before_any_hip_call(entry, which):
+    """Both fused entry points (plain and transposed D) reject every NULL array
+    with ERR_INVALID_ARG.  On this GPU-less host any HIP call would fail with
+    ERR_HIP instead, so the status shows that the check precedes all device
+    work (the transposed-D call allocates and transposes only afterwards)."""
+    names = ["rowptr", "colidx", "vals", "C", "D", "E", "A"]
+    args = [NULL if n == which else FAKE for n in names]
+    fn = getattr(slnr.lib(), entry)
+    assert fn(*args, 64, 48, 16, 32, NULL) == slnr.ERR_INVALID_ARG
+    # the same call with every pointer set gets past the checks to the HIP
+    # runtime, which fails without a GPU: the checks alone made the difference
+    if not _gpu_visible():
+        assert fn(*(FAKE,) * 7, 64, 48, 16, 32, NULL) == slnr.ERR_HIP
+
+
+def _gpu_visible():
+    """True where a GPU may be present (then the fake pointers must never
+    reach a launch).  Counting devices does not initialise HIP."""
+    if os.path.exists("/dev/kfd"):
+        return True
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return True
+
+
 def test_header_is_plain_c(tmp_path):
     """The header and the C caller compile as C11 (no C++ in the interface)."""
     import subprocess

@@ -9,7 +9,7 @@ import pytest
 import oracle
 import paper_2205_11622_amd as slnr
 import synth
-from tests.gpu_util import make_problem, power_law_lengths, sample_rows
+from tests.gpu_util import make_problem, oracle_reference, power_law_lengths, rows_close_dev
 from tests.parity import assert_rows_close
 
 pytestmark = pytest.mark.gpu
@@ -188,48 +188,54 @@ def test_next_grid_factors(gpu, factor):
 @pytest.mark.parametrize("kernel", ["sddmm_spmm_gemm", "spmm_gemm", "spmmh_gemm", "dt"])
 def test_next_on_rmat1m(gpu, kernel):
     """The R-MAT 2^20 structure at the inner sizes the paper uses for each
-    benchmark (K=L=M=64; K=128, L=64; J=L=128), sampled rows, at every grid
-    factor the benchmark may time and at the automatic one."""
+    benchmark (K=L=M=64; K=128, L=64; J=L=128; D transposed at K=L=128):
+    every row, at every grid factor the benchmark may time and at the
+    automatic one.  The output is NaN-filled before each call, so a row left
+    unwritten fails."""
     import torch
 
     import bench
     base = synth.config("rmat1m")
-    rows = sample_rows(base, n_random=1500)
     rp, ci, v = csr(base)
+    r3 = (base.rowptr, base.colidx, base.vals)
     if kernel == "sddmm_spmm_gemm":
         C, D, F = (synth.normal(0, s, (base.N, 64)) for s in (3, 4, 5))
         W = synth.normal(0, 6, (64, 64))
         args = (rp, ci, v, dev(C), dev(D), dev(F), dev(W))
         call = slnr.sparselnr_fused_sddmm_spmm_gemm
-        ref, scale, _ = oracle.sddmm_spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, F,
-                                                    W, rows=rows)
+        fn = lambda rows: oracle.sddmm_spmm_gemm_rows(*r3, C, D, F, W, rows=rows)  # noqa: E731
+        width = 64
     elif kernel == "spmm_gemm":
         C, Dk = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 6, (128, 64))
         args = (rp, ci, v, dev(C), dev(Dk))
         call = slnr.sparselnr_spmm_gemm
-        ref, scale, _ = oracle.spmm_gemm_rows(base.rowptr, base.colidx, base.vals, C, Dk,
-                                              rows=rows)
+        fn = lambda rows: oracle.spmm_gemm_rows(*r3, C, Dk, rows=rows)  # noqa: E731
+        width = 64
     elif kernel == "spmmh_gemm":
         C, D = synth.normal(0, 4, (base.N, 128)), synth.normal(0, 5, (base.N, 128))
         E = synth.normal(0, 6, (128, 128))
         args = (rp, ci, v, dev(C), dev(D), dev(E))
         call = slnr.sparselnr_spmmh_gemm
-        ref, scale, _ = oracle.spmmh_gemm_rows(base.rowptr, base.colidx, base.vals, C, D, E,
-                                               rows=rows)
+        fn = lambda rows: oracle.spmmh_gemm_rows(*r3, C, D, E, rows=rows)  # noqa: E731
+        width = 128
     else:
         Dt = np.ascontiguousarray(base.D.T)
         args = (rp, ci, v, dev(base.C), dev(Dt), dev(base.E))
         call = slnr.sparselnr_fused_sddmm_spmm_dt
-        ref, scale, _ = oracle.fused_rows_dt(base.rowptr, base.colidx, base.vals, base.C, Dt,
-                                             base.E, rows=rows)
+        fn = lambda rows: oracle.fused_rows_dt(*r3, base.C, Dt, base.E, rows=rows)  # noqa: E731
+        width = base.L
+    print("rmat1m %s: N=%d nnz=%d" % (kernel, base.N, base.nnz), flush=True)
+    ref, scale = oracle_reference(fn, base.N, width, gpu)
+    A = torch.empty((base.N, width), dtype=torch.float32, device=gpu)
     try:
         for f in (0,) + tuple(bench.GRID_FACTORS):
             slnr.sparselnr_set_grid_factor(f)
-            A = call(*args)
-            assert_rows_close(rows_of(A, rows), ref, scale,
-                              what="%s, grid factor %s" % (kernel, f or "automatic"))
-            assert not bool(torch.isnan(A).any())
+            what = "%s, grid factor %s" % (kernel, f or "automatic")
+            A.fill_(float("nan"))
+            call(*args, A=A)
+            w = rows_close_dev(A, ref, scale, what=what)
+            print("  %s: worst err/scale %.2e" % (what, w), flush=True)
     finally:
         slnr.sparselnr_set_grid_factor(0)
-    del A
+    del A, ref, scale
     torch.cuda.empty_cache()

@@ -11,8 +11,8 @@ import pytest
 import oracle
 import paper_2205_11622_amd as slnr
 import synth
-from tests.gpu_util import (check_A_rows, check_Y, fused, make_problem, power_law_lengths,
-                            sample_rows, unfused, upload)
+from tests.gpu_util import (check_A_rows, check_Y, fused, fused_reference, make_problem,
+                            power_law_lengths, rows_close_dev, sample_rows, unfused, upload)
 from tests.parity import assert_rows_close
 
 pytestmark = pytest.mark.gpu
@@ -431,35 +431,37 @@ def test_config_full(gpu, name):
 
 @pytest.mark.slow
 @pytest.mark.parametrize("name", ["rmat1m", "rmat4m", "banded"])
-def test_config_sampled(gpu, name):
-    # full size, at every grid factor the benchmark may time (it picks one
-    # per call from bench.GRID_FACTORS), and at the automatic one
+def test_config_every_row(gpu, name):
+    # Full size, every row of A and every SDDMM value (the fused and the
+    # separate forms compute the same result: Section 3.1, Figure 2), at the
+    # automatic grid factor and at every factor the benchmark may time (it
+    # picks one per call from bench.GRID_FACTORS).  Outputs are NaN-filled
+    # before each call, so a row left unwritten fails.
     import torch
 
     import bench
     p = synth.config(name)
+    print("%s: N=%d nnz=%d K=%d L=%d" % (name, p.N, p.nnz, p.K, p.L), flush=True)
+    ref, scale, Yref, Yscale = fused_reference(p, gpu)
     d = upload(p)
-    rows = sample_rows(p)
-    yrows = rows[:500]
-    ref, scale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E, rows=rows)
-    _, _, Yref, Yscale, _ = oracle.fused_rows(p.rowptr, p.colidx, p.vals, p.C, p.D, p.E,
-                                              rows=yrows, with_y=True)
-    yidx = torch.from_numpy(np.concatenate(
-        [np.arange(p.rowptr[i], p.rowptr[i + 1]) for i in yrows])).to(gpu)
-    rsel = torch.from_numpy(rows).to(gpu)
+    A = torch.empty((p.N, p.L), dtype=torch.float32, device=gpu)
+    Au = torch.empty_like(A)
+    Y = torch.empty(p.nnz, dtype=torch.float32, device=gpu)
+    args = (d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"])
     try:
         for f in (0,) + tuple(bench.GRID_FACTORS):
             slnr.sparselnr_set_grid_factor(f)
             what = "%s, grid factor %s" % (name, f or "automatic")
-            assert_rows_close(fused(d)[rsel].cpu().numpy(), ref, scale, what=what + ", fused")
-            Y, Au = unfused(d)
-            assert_rows_close(Y[yidx].cpu().numpy(), Yref, Yscale, what=what + ", Y")
-            assert_rows_close(Au[rsel].cpu().numpy(), ref, scale, what=what + ", unfused")
+            for t in (A, Au, Y):
+                t.fill_(float("nan"))
+            slnr.sparselnr_fused_sddmm_spmm(*args, A=A)
+            slnr.sparselnr_unfused_sddmm_spmm(*args, Y=Y, A=Au)
+            w = rows_close_dev(A, ref, scale, what=what + ", fused")
+            wy = rows_close_dev(Y, Yref, Yscale, what=what + ", Y")
+            wu = rows_close_dev(Au, ref, scale, what=what + ", unfused")
+            print("  %s: worst err/scale fused %.2e, Y %.2e, unfused %.2e" % (what, w, wy, wu),
+                  flush=True)
     finally:
         slnr.sparselnr_set_grid_factor(0)
-    # every row of A written: no NaN left from a NaN-filled output
-    A = torch.full((p.N, p.L), float("nan"), device=gpu)
-    slnr.sparselnr_fused_sddmm_spmm(d["rowptr"], d["colidx"], d["vals"], d["C"], d["D"], d["E"], A)
-    assert not bool(torch.isnan(A).any())
-    del A, Y, Au, d
+    del A, Au, Y, d, ref, scale, Yref, Yscale
     torch.cuda.empty_cache()

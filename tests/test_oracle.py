@@ -265,6 +265,49 @@ def test_scale_bounds_and_nonnegative_case():
     assert np.allclose(Ap.max(axis=1), sp, rtol=1e-13, atol=0)
 
 
+def test_scale_outputs_match_dense_absolute_products():
+    """Every tolerance scale the oracle returns is its definition on absolute
+    values, written here as dense numpy products on small integers (exact in
+    fp64): the SDDMM scale |b_p| (|C| |D|^T)[i, j]; the SpMM scale
+    max_l (S |E|)[i, l] with S[i, j] the sum of the Yabs of row i's nonzeros
+    in column j; and the fused scale max_l ((|B| .* (|C| |D|^T)) |E|)[i, l].
+    The inputs have negative entries in every operand and rows whose column
+    sums differ, so a dropped absolute value, a sum over l in place of the
+    maximum, or a transposed operand changes the result."""
+    rng = np.random.default_rng(21)
+    N, M, K, L = 40, 30, 5, 7
+    rp, ci = random_csr(rng, N, M, 9, allow_dups=True, shuffle=True)
+    v = ints(rng, ci.size)
+    C, D, E = ints(rng, (N, K)), ints(rng, (M, K)), ints(rng, (M, L))
+    assert (v < 0).any() and (C < 0).any() and (D < 0).any() and (E < 0).any()
+    Ba = dense_B(rp, ci, np.abs(v), M)
+    Ta = np.abs(C).astype(np.float64) @ np.abs(D).astype(np.float64).T
+    rows = np.repeat(np.arange(N), np.diff(rp))
+    # SDDMM scale per nonzero
+    Y, Yscale, _ = oracle.sddmm(rp, ci, v, C, D, with_scale=True)
+    assert np.array_equal(Yscale, np.abs(v).astype(np.float64) * Ta[rows, ci])
+    # SpMM scale per row, from an arbitrary nonnegative Yabs (integers)
+    Yabs = rng.integers(0, 5, size=ci.size).astype(np.float64)
+    S = np.zeros((N, M))
+    np.add.at(S, (rows, ci), Yabs)
+    full = S @ np.abs(E).astype(np.float64)
+    A, Ascale, _ = oracle.spmm(rp, ci, Y, E, Yabs=Yabs)
+    assert np.array_equal(Ascale, full.max(axis=1))
+    # the planted slips give other values on these inputs
+    assert not np.array_equal(Ascale, full.sum(axis=1))
+    assert not np.array_equal(Ascale, (S @ E.astype(np.float64)).max(axis=1))
+    # the values themselves are unchanged by asking for the scale
+    A0, _ = oracle.spmm(rp, ci, Y, E)
+    assert np.array_equal(A, A0)
+    # fused scale per row
+    Afull = (Ba * Ta) @ np.abs(E).astype(np.float64)
+    _, scale, _ = oracle.fused_rows(rp, ci, v, C, D, E)
+    assert np.array_equal(scale, Afull.max(axis=1))
+    # and the SpMM scale carried from the SDDMM scale equals the fused one
+    _, As2, _ = oracle.spmm(rp, ci, Y, E, Yabs=Yscale)
+    assert np.array_equal(As2, scale)
+
+
 def test_subset_rows_match_full():
     rng = np.random.default_rng(15)
     N, M, K, L = 80, 70, 8, 8
