@@ -27,18 +27,9 @@ constexpr int kBlock = 256;       // threads per block (4 waves)
 // (uniform 65536 x 16: fused +1.5%, unfused -1.4%).  Smaller blocks leave the
 // dispatcher a finer-grained tail and spread each XCD's share more evenly.
 constexpr int kWalkBlock = 64;
-#ifndef SLNR_MIN_CHUNK
-#define SLNR_MIN_CHUNK 64
-#endif
-constexpr int kMinChunk = SLNR_MIN_CHUNK;  // smallest merge-path slice per worker
+constexpr int kMinChunk = 64;     // smallest merge-path slice per worker
 constexpr int kXcds = 8;          // MI355X deals blocks over 8 XCDs
-#ifndef SLNR_GRID_FACTOR
-#define SLNR_GRID_FACTOR 8
-#endif
-#ifndef SLNR_XCD_REMAP
-#define SLNR_XCD_REMAP 1
-#endif
-constexpr int kGridFactor = SLNR_GRID_FACTOR;
+constexpr int kGridFactor = 8;    // resident grids per walk launch for large inputs
 constexpr int kGenericLT = 4;     // generic path: 4 x 64 = 256 columns per tile
 // <SpMMH, GEMM>: C .* D is formed once when nnz >= kHoistRatio * M (12 M J
 // bytes for the product against 4 J bytes per nonzero for a second gather).
@@ -189,30 +180,15 @@ Variant generic() {
 // see with_fine), the unfused ones pipeline them.  Nonzeros per
 // step of the paced schedule: 8 for the 128-wide rows, 4 otherwise (the
 // 64-lane kernels of large inputs take their own, below).
-#ifndef SLNR_FUSED_SCHED
-#define SLNR_FUSED_SCHED 1
-#endif
-#ifndef SLNR_UNFUSED_SCHED
-#define SLNR_UNFUSED_SCHED 0
-#endif
-#ifndef SLNR_PACED_U
-#define SLNR_PACED_U 4
-#endif
-#ifndef SLNR_PACED_U128
-#define SLNR_PACED_U128 8
-#endif
-constexpr int kFS = SLNR_FUSED_SCHED;
-constexpr int kUS = SLNR_UNFUSED_SCHED;
-constexpr int kPU = SLNR_PACED_U;
-constexpr int kPU128 = SLNR_PACED_U128;
+constexpr int kFS = slnr::kPaced;
+constexpr int kUS = slnr::kPipelined;
+constexpr int kPU = 4;
+constexpr int kPU128 = 8;
 
 // Inputs that fit one resident grid (few rows per worker) run with more
 // nonzeros per paced step at K = L = 32 and 64 (measured on MI355X: 8 per step
 // is 8% faster on 65536 rows of 16 nonzeros, 4 is 1% faster on R-MAT 2^22).
-#ifndef SLNR_PACED_U_SMALL
-#define SLNR_PACED_U_SMALL 8
-#endif
-constexpr int kPUs = SLNR_PACED_U_SMALL;
+constexpr int kPUs = 8;
 
 // The 64-lane fused kernel of large inputs at K = L = 128 takes 10 nonzeros
 // per paced step (measured on MI355X, R-MAT 2^20: 1.5-2.3% faster than 8 on
@@ -438,7 +414,7 @@ Grid make_grid(int cus, int per_cu, int block, int W, int64_t N, int factor = 0)
   blocks = ((blocks + kXcds - 1) / kXcds) * kXcds;
   g.blocks = blocks;
   g.workers = blocks * (block / 64) * (64 / W);
-  g.xcd_span = SLNR_XCD_REMAP ? blocks / kXcds : 0;
+  g.xcd_span = blocks / kXcds;  // XCD-contiguous slice numbering
   g.factor = factor;
   return g;
 }

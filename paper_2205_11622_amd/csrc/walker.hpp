@@ -27,14 +27,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#ifndef SLNR_NT
-#define SLNR_NT 1
-#endif
-
 namespace slnr {
 
-// Streams read or written once per call carry the nontemporal hint.
-constexpr bool kNT = SLNR_NT != 0;
+// Streams read or written once per call carry the nontemporal hint (C, the
+// CSR arrays, A).  Measured on MI355X against plain loads and stores: the
+// fused walk is 0.5-1.5% faster with the hint, the unfused passes 0.4-2%.
+constexpr bool kNT = true;
 
 enum Mode : int { kFused = 0, kSddmm = 1, kSpmm = 2 };
 

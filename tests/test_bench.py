@@ -48,3 +48,27 @@ def test_byte_model_matches_its_formula():
     N, K, L, nnz = p.N, p.K, p.L, p.nnz
     assert nnz == 20480
     assert p.model_bytes() == 4 * (N + 1) + 8 * nnz + 4 * nnz * (K + L) + 4 * N * K + 4 * N * L
+
+
+def test_row_parity_rule_of_the_bench_line():
+    """bench.row_parity applies the tests' per-row rule (tests/parity.py)."""
+    import numpy as np
+
+    import bench
+    from tests.parity import row_errors
+    rng = np.random.default_rng(4)
+    ref = rng.standard_normal((500, 6))
+    scale = np.abs(ref).max(axis=1) * 1.5
+    got = (ref * (1 + 1e-6 * rng.standard_normal(ref.shape))).astype(np.float32)
+    scale[:4] = 0.0
+    ref[:4] = 0.0
+    got[:3] = 0.0
+    got[3, 0] = 1e-20          # nonzero in a zero-scale row
+    got[9, 2] = np.nan
+    got[17] += 1e-3 * scale[17]
+    worst, bad = bench.row_parity(got, ref, scale, chunk=64)
+    _, ratio = row_errors(got, ref, scale)
+    assert bad == int((~(ratio <= 1e-4)).sum()) == 3
+    assert worst == np.inf
+    worst_ok, bad_ok = bench.row_parity(got[20:], ref[20:], scale[20:], chunk=64)
+    assert bad_ok == 0 and worst_ok == ratio[20:].max()
