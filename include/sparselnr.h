@@ -109,6 +109,36 @@ SPARSELNR_API int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_
                                              int64_t N, int64_t M, int64_t K, int64_t L,
                                              void *stream);
 
+/* Size in bytes of the device array of sparselnr_fused_sddmm_spmm_noalloc. */
+#define SPARSELNR_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * computation, arguments, layouts and argument errors as
+ * sparselnr_fused_sddmm_spmm, with no allocation of any kind (no hipMalloc,
+ * hipFree or allocating library routine).  The partial rows of rows split
+ * between workers go to a fixed device array of
+ * SPARSELNR_NOALLOC_SCRATCH_BYTES (64 MiB) inside the library, one per GPU,
+ * held from the first call on that GPU until the process ends.  The call
+ * runs at the grid factor the fused entry point would use, halved until the
+ * partial rows fit the array (so results may differ from the fused entry
+ * point's in rounding order, within its accuracy; they are bit-identical
+ * when the same factor fits, as it does at the automatic factor for the
+ * workloads of this library).  It returns SPARSELNR_ERR_UNSUPPORTED if they
+ * do not fit even at one resident grid (not reached for K, L <= 512).
+ * All calls on one GPU share that GPU's array and it keeps the last call's
+ * contents: calls that overlap in time on one GPU (different streams, or
+ * different host threads) RACE and corrupt each other's results; order them
+ * on one stream.  Nothing in the array needs clearing between calls.
+ */
+SPARSELNR_API int sparselnr_fused_sddmm_spmm_noalloc(const int32_t *rowptr,
+                                                     const int32_t *colidx, const float *vals,
+                                                     const float *C, const float *D,
+                                                     const float *E, float *A, int64_t N,
+                                                     int64_t M, int64_t K, int64_t L,
+                                                     void *stream);
+
 /*
  * Unfused comparison (Figure 2a then Figure 2b, Section 3.1.2): the SDDMM
  * writes Y (nnz floats, structure of B, same order as colidx), then the SpMM

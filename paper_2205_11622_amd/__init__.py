@@ -22,7 +22,8 @@ LIB_PATH = os.path.join(_PKG, "libsparselnr.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NO_MEMORY, ERR_INVALID_CSR = range(6)
 
 __all__ = [
-    "sparselnr_fused_sddmm_spmm", "sparselnr_unfused_sddmm_spmm", "sparselnr_sddmm",
+    "sparselnr_fused_sddmm_spmm", "sparselnr_fused_sddmm_spmm_noalloc",
+    "sparselnr_unfused_sddmm_spmm", "sparselnr_sddmm",
     "sparselnr_spmm", "sparselnr_fused_sddmm_spmm_gemm", "sparselnr_spmm_gemm",
     "sparselnr_spmmh_gemm", "sparselnr_fused_sddmm_spmm_dt", "sparselnr_validate_csr", "sparselnr_release", "sparselnr_status_string",
     "sparselnr_last_hip_error", "sparselnr_abi_version", "sparselnr_set_grid_factor",
@@ -53,6 +54,8 @@ def lib() -> ctypes.CDLL:
         vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
         L.sparselnr_fused_sddmm_spmm.argtypes = [vp] * 7 + [i64] * 4 + [vp]
         L.sparselnr_fused_sddmm_spmm.restype = ci
+        L.sparselnr_fused_sddmm_spmm_noalloc.argtypes = [vp] * 7 + [i64] * 4 + [vp]
+        L.sparselnr_fused_sddmm_spmm_noalloc.restype = ci
         L.sparselnr_unfused_sddmm_spmm.argtypes = [vp] * 8 + [i64] * 4 + [vp]
         L.sparselnr_unfused_sddmm_spmm.restype = ci
         L.sparselnr_sddmm.argtypes = [vp] * 6 + [i64] * 3 + [vp]
@@ -200,6 +203,27 @@ def sparselnr_fused_sddmm_spmm(rowptr, colidx, vals, C, D, E, A=None, stream=Non
         _ptr(D, device), _ptr(E, device), _ptr(A, device), N, M, K, L, _stream(stream, device))
     if rc != OK:
         raise SparseLNRError(rc, "sparselnr_fused_sddmm_spmm")
+    return A
+
+
+def sparselnr_fused_sddmm_spmm_noalloc(rowptr, colidx, vals, C, D, E, A, stream=None):
+    """The fused call for callers that cannot allocate: A (N x L) must be
+    given; the library uses a fixed device array for split rows.  Calls that
+    overlap on one GPU race (see include/sparselnr.h)."""
+    torch = _torch()
+    device, N = _csr(rowptr, colidx, vals)
+    K = _dense(C, "C", N, device)
+    M = D.shape[0] if isinstance(D, torch.Tensor) and D.dim() == 2 else -1
+    if _dense(D, "D", M, device) != K:
+        raise ValueError("C and D differ in width K")
+    L = _dense(E, "E", M, device)
+    if A is None or _dense(A, "A", N, device) != L:
+        raise ValueError("A must be given, N x L")
+    rc = lib().sparselnr_fused_sddmm_spmm_noalloc(
+        _ptr(rowptr, device), _ptr(colidx, device), _ptr(vals, device), _ptr(C, device),
+        _ptr(D, device), _ptr(E, device), _ptr(A, device), N, M, K, L, _stream(stream, device))
+    if rc != OK:
+        raise SparseLNRError(rc, "sparselnr_fused_sddmm_spmm_noalloc")
     return A
 
 

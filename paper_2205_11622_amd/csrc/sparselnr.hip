@@ -437,16 +437,13 @@ FixupShape fixup_shape(int cus, int64_t workers) {
   return FixupShape{(int)(blocks > 0 ? blocks : 1), G};
 }
 
-// Runs one merge-path walk (+ carry fixup unless SDDMM) over the whole matrix.
-// With nv > 1, the variants are gated alternatives, each with its own
-// arguments as[k] (only the one whose gate opens on the device does any
-// work): they share one grid, workspace and slice split, so the one carry
-// fixup serves whichever ran.
-int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream_t stream) {
-  WalkArgs a = as[0];
-  int dev = 0, cus = 0, rc;
-  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
-  if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
+// Kernel and grid of a walk launch at a requested grid factor (0: the
+// automatic or process-wide choice): one resident grid takes the
+// small-input kernel, several the wide-worker kernel, fine slices the
+// fine-slice kernel, where the variant has them.
+int choose_launch(int dev, int cus, const Variant *vs, int nv, int64_t N, int factor,
+                  Variant *v_out, Grid *g_out) {
+  int rc;
   Variant v = vs[0];
   int per_cu = 1;
   if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
@@ -458,35 +455,84 @@ int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream
       return rc;
     if (pc < per_cu) per_cu = pc;
   }
-  Grid g = make_grid(cus, per_cu, v.block, v.W, a.N);
+  Grid g = make_grid(cus, per_cu, v.block, v.W, N, factor);
   if (nv == 1 && g.factor == 1 && v.fn_small) {  // one resident grid: the small-input schedule
     v.fn = v.fn_small;
     if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
-    g = make_grid(cus, per_cu, v.block, v.W, a.N);
+    g = make_grid(cus, per_cu, v.block, v.W, N, factor);
   } else if (nv == 1 && g.factor > 1 && v.fn_wide) {  // several grids: the wide workers
     v.fn = v.fn_wide;
     v.W = v.W_wide;
     if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
-    g = make_grid(cus, per_cu, v.block, v.W, a.N, g.factor);
+    g = make_grid(cus, per_cu, v.block, v.W, N, g.factor);
   } else if (nv == 1 && v.fn_fine && g.factor >= v.fine_factor) {  // fine slices
     v.fn = v.fn_fine;
     if ((rc = blocks_per_cu(dev, v.fn, v.block, v.lds, &per_cu)) != SPARSELNR_OK) return rc;
-    g = make_grid(cus, per_cu, v.block, v.W, a.N, g.factor);
+    g = make_grid(cus, per_cu, v.block, v.W, N, g.factor);
+  }
+  *v_out = v;
+  *g_out = g;
+  return SPARSELNR_OK;
+}
+
+// Carry workspace of a walk launch: two partial rows of the l-tile width
+// plus two int32 of metadata per worker.
+struct CarrySize {
+  size_t carry, meta;
+  size_t total() const { return carry + meta; }
+};
+
+CarrySize carry_size(const Grid &g, int64_t tile_w) {
+  return CarrySize{(size_t)g.workers * 2 * (size_t)tile_w * sizeof(float),
+                   (size_t)g.workers * 2 * sizeof(int32_t)};
+}
+
+// A buffer the caller provides instead of the per-(device, stream)
+// workspace (the no-allocation entry point): its device address and size.
+struct FixedBuffer {
+  void *ptr;
+  size_t bytes;
+};
+
+// Runs one merge-path walk (+ carry fixup unless SDDMM) over the whole matrix.
+// With nv > 1, the variants are gated alternatives, each with its own
+// arguments as[k] (only the one whose gate opens on the device does any
+// work): they share one grid, workspace and slice split, so the one carry
+// fixup serves whichever ran.  With `fixed`, the partial rows go to that
+// buffer instead of the workspace, and the grid factor is halved until they
+// fit (ERR_UNSUPPORTED if they do not fit at one resident grid); the walk
+// then allocates nothing.
+int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream_t stream,
+             const FixedBuffer *fixed = nullptr) {
+  WalkArgs a = as[0];
+  int dev = 0, cus = 0, rc;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  if ((rc = device_cus(dev, &cus)) != SPARSELNR_OK) return rc;
+  Variant v;
+  Grid g;
+  if ((rc = choose_launch(dev, cus, vs, nv, a.N, 0, &v, &g)) != SPARSELNR_OK) return rc;
+  const int64_t tiles = vs[0].generic ? (a.L + 64 * kGenericLT - 1) / (64 * kGenericLT) : 1;
+  const int64_t tile_w = vs[0].generic ? 64 * kGenericLT : a.L;
+  if (fixed && mode != kSddmm) {
+    while (carry_size(g, tile_w).total() > fixed->bytes && g.factor > 1)
+      if ((rc = choose_launch(dev, cus, vs, nv, a.N, g.factor / 2, &v, &g)) != SPARSELNR_OK)
+        return rc;
+    if (carry_size(g, tile_w).total() > fixed->bytes) return SPARSELNR_ERR_UNSUPPORTED;
   }
   a.workers = g.workers;
   a.min_chunk = kMinChunk;
   a.xcd_span = g.xcd_span;
   a.xcds = kXcds;
-  const int64_t tiles = v.generic ? (a.L + 64 * kGenericLT - 1) / (64 * kGenericLT) : 1;
-  const int64_t tile_w = v.generic ? 64 * kGenericLT : a.L;
   if (mode != kSddmm) {
-    const size_t carry_bytes = (size_t)g.workers * 2 * (size_t)tile_w * sizeof(float);
-    const size_t meta_bytes = (size_t)g.workers * 2 * sizeof(int32_t);
+    const CarrySize cs = carry_size(g, tile_w);
     void *ws = nullptr;
-    if ((rc = get_workspace(dev, stream, carry_bytes + meta_bytes, &ws)) != SPARSELNR_OK)
+    if (fixed) {
+      ws = fixed->ptr;
+    } else if ((rc = get_workspace(dev, stream, cs.total(), &ws)) != SPARSELNR_OK) {
       return rc;
+    }
     a.carry = (float *)ws;
-    a.meta = (int32_t *)((char *)ws + carry_bytes);
+    a.meta = (int32_t *)((char *)ws + cs.carry);
   } else {
     a.carry = nullptr;
     a.meta = nullptr;
@@ -519,8 +565,9 @@ int run_walk(Mode mode, const Variant *vs, const WalkArgs *as, int nv, hipStream
   return SPARSELNR_OK;
 }
 
-int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream) {
-  return run_walk(mode, &v, &a, 1, stream);
+int run_walk(Mode mode, const Variant &v, WalkArgs a, hipStream_t stream,
+             const FixedBuffer *fixed = nullptr) {
+  return run_walk(mode, &v, &a, 1, stream, fixed);
 }
 
 bool bad_size(int64_t N, int64_t M, int64_t K, int64_t L) {
@@ -545,6 +592,36 @@ int check_fused_args(const int32_t *rowptr, const int32_t *colidx, const float *
   if (N > 0 && M > 0 && L > 0 && !E) return SPARSELNR_ERR_INVALID_ARG;
   if (N > 0 && L > 0 && !A) return SPARSELNR_ERR_INVALID_ARG;
   return check_range(N, M, K, L);
+}
+
+// Device array of the no-allocation fused entry point: the partial rows of
+// split rows and their metadata.  Each GPU the library runs on holds one copy
+// for the life of the process.  Host code never uses the name `scratch` as
+// an address: the device address of each GPU's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kScratchBytes = SPARSELNR_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes % 256 == 0, "scratch size");
+constexpr int kMaxDevices = 64;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+namespace {
+
+int scratch_address(int dev, void **out) {
+  if (dev < 0 || dev >= kMaxDevices) return SPARSELNR_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e);
+    if (!p) return hip_fail(hipErrorInvalidSymbol);
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SPARSELNR_OK;
 }
 
 WalkArgs base_args(const int32_t *rowptr, const int32_t *colidx, const float *vals,
@@ -634,6 +711,27 @@ int sparselnr_fused_sddmm_spmm(const int32_t *rowptr, const int32_t *colidx,
   a.E = E;
   a.out = A;
   return run_walk(kFused, pick_fused(K, L, al), a, (hipStream_t)stream);
+}
+
+int sparselnr_fused_sddmm_spmm_noalloc(const int32_t *rowptr, const int32_t *colidx,
+                                       const float *vals, const float *C, const float *D,
+                                       const float *E, float *A, int64_t N, int64_t M,
+                                       int64_t K, int64_t L, void *stream) {
+  int rc = check_fused_args(rowptr, colidx, vals, C, D, E, A, N, M, K, L);
+  if (rc != SPARSELNR_OK) return rc;
+  if (N == 0 || L == 0) return SPARSELNR_OK;
+  const bool al = aligned16(C) && aligned16(D) && aligned16(E) && aligned16(A) &&
+                  offsets32(M, K) && offsets32(M, L);
+  int dev = 0;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  FixedBuffer fb{nullptr, kScratchBytes};
+  if ((rc = scratch_address(dev, &fb.ptr)) != SPARSELNR_OK) return rc;
+  WalkArgs a = base_args(rowptr, colidx, vals, N, K, L);
+  a.C = C;
+  a.D = D;
+  a.E = E;
+  a.out = A;
+  return run_walk(kFused, pick_fused(K, L, al), a, (hipStream_t)stream, &fb);
 }
 
 int sparselnr_sddmm(const int32_t *rowptr, const int32_t *colidx, const float *vals,

@@ -188,7 +188,8 @@ def test_next_entry_points_argument_errors():
     assert L.sparselnr_fused_sddmm_spmm_dt(*(FAKE,) * 7, -4, 4, 4, 4, NULL) == slnr.ERR_INVALID_ARG
 
 
-@pytest.mark.parametrize("entry", ["sparselnr_fused_sddmm_spmm", "sparselnr_fused_sddmm_spmm_dt"])
+@pytest.mark.parametrize("entry", ["sparselnr_fused_sddmm_spmm", "sparselnr_fused_sddmm_spmm_dt",
+                                   "sparselnr_fused_sddmm_spmm_noalloc"])
 @pytest.mark.parametrize("which", ["rowptr", "colidx", "vals", "C", "D", "E", "A"])
 def test_fused_null_pointer_rejected_before_any_hip_call(entry, which):
     """Both fused entry points (plain and transposed D) reject every NULL array
