@@ -29,8 +29,15 @@ namespace slnr {
 // stored by 64 lanes in one coalesced pass per 64 columns.  Wep is read
 // through the caches (it is small and every wave reads it), which leaves LDS
 // to the tiles.
-template <int MODE, int W, int LV, int HAD, int TR, int SCHED, int U>
-__global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
+//
+// With WL = 1 the block first copies the whole Wep into LDS (one copy shared
+// by the block's waves, which are then many: the host launches up to 16
+// waves per block) and the tile products read it from there; otherwise they
+// read it through the caches.  LDS layout: [Wep, Lin x Lout floats rounded
+// up to a multiple of 4] [tiles, TR rows of TS floats per wave]
+// [destinations, TR per wave].
+template <int MODE, int W, int LV, int HAD, int TR, int SCHED, int U, int WL = 0>
+__global__ __launch_bounds__(WL ? 1024 : 256) void walk_epi(WalkArgs a) {
   constexpr int KV = LV;  // fused form: K = Lin
   constexpr int LIN = W * LV;
   constexpr int WPW = 64 / W;  // workers per wave
@@ -43,10 +50,18 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
   const int glane = lane & (W - 1);
   const int gbase = lane - glane;
   const int wave = threadIdx.x >> 6;
-  float *tile = smem + wave * (TR * TS);
-  uint64_t *tdst = reinterpret_cast<uint64_t *>(smem + (blockDim.x >> 6) * (TR * TS)) + wave * TR;
+  const int wsize = WL ? ((LIN * a.L + 3) & ~3) : 0;  // floats of the staged Wep
+  float *wlds = smem;
+  float *tile = smem + wsize + wave * (TR * TS);
+  uint64_t *tdst =
+      reinterpret_cast<uint64_t *>(smem + wsize + (blockDim.x >> 6) * (TR * TS)) + wave * TR;
 
   if (gate_closed(a.gate, a.rowptr, a.N, a.gate_nnz)) return;
+  if constexpr (WL) {  // the whole block takes part (the gate is uniform over the grid)
+    const int n = LIN * a.L;
+    for (int t = threadIdx.x; t < n; t += blockDim.x) wlds[t] = a.Wep[t];
+    __syncthreads();
+  }
   const Slice s = make_slice<W>(a);
   const int64_t worker = s.id;
   RowWalk<MODE, W, 1, KV, LV, SCHED, U, HAD> rw(a, s.p1, (uint32_t)LIN * 4u);
@@ -71,7 +86,8 @@ __global__ __launch_bounds__(256) void walk_epi(WalkArgs a) {
     const float *arow = tile + (lane & 3) * TS;
     for (int c0 = 0; c0 < lout; c0 += 64) {
       const int col = c0 + lane;
-      const float *wcol = Wm + (col < lout ? col : c0);  // lanes past Lout read a valid column
+      const int wc = col < lout ? col : c0;  // lanes past Lout read a valid column
+      const float *wcol = WL ? wlds + wc : Wm + wc;
       f4_t o[TR / 4];
 #pragma unroll
       for (int q = 0; q < TR / 4; ++q) o[q] = f4_t{0.f, 0.f, 0.f, 0.f};

@@ -47,7 +47,7 @@ struct Workspace {
 
 std::mutex g_mu;
 std::map<int, int> g_cus;                                    // device -> CUs
-std::map<std::pair<int, uintptr_t>, int> g_occupancy;        // (device, kernel) -> blocks/CU
+std::map<std::pair<int, std::pair<uintptr_t, size_t>>, int> g_occupancy;  // (device, (kernel, LDS)) -> blocks/CU
 // Resident grids per walk launch: 0 not read yet (SPARSELNR_GRID_FACTOR gives
 // the first value), -1 chosen per call by size, 1..kMaxGridFactor fixed
 // (sparselnr_set_grid_factor).
@@ -70,6 +70,23 @@ std::map<WsKey, Workspace> g_workspace;
 int current_device(int *dev) {
   hipError_t e = hipGetDevice(dev);
   if (e != hipSuccess) return hip_fail(e);
+  return SPARSELNR_OK;
+}
+
+std::map<int, size_t> g_max_lds;  // device -> largest LDS of one block
+
+int device_max_lds(int dev, size_t *out) {
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_max_lds.find(dev);
+  if (it != g_max_lds.end()) {
+    *out = it->second;
+    return SPARSELNR_OK;
+  }
+  int n = 0;
+  hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return hip_fail(e);
+  g_max_lds[dev] = n > 0 ? (size_t)n : 0;
+  *out = g_max_lds[dev];
   return SPARSELNR_OK;
 }
 
@@ -162,6 +179,23 @@ Variant epi() {
   v.generic = false;
   constexpr int TS = W * LV + 4;
   v.lds = (size_t)(kBlock / 64) * TR * (TS * sizeof(float) + sizeof(uint64_t));
+  return v;
+}
+
+// The same with the dense matrix staged in LDS once per block of `block`
+// threads (Lin x Lout floats, Lout known per call).
+template <int MODE, int W, int LV, int HAD, int TR>
+Variant epi_wl(int64_t Lout, int block) {
+  Variant v;
+  v.fn = slnr::walk_epi<MODE, W, LV, HAD, TR, slnr::kPipelined, 1, 1>;
+  v.W = W;
+  v.generic = false;
+  v.block = block;
+  constexpr int LIN = W * LV;
+  constexpr int TS = LIN + 4;
+  const size_t wfloats = ((size_t)LIN * Lout + 3) & ~(size_t)3;
+  v.lds = wfloats * sizeof(float) + (size_t)(block / 64) * TR * (TS * sizeof(float) +
+                                                                   sizeof(uint64_t));
   return v;
 }
 
@@ -352,15 +386,55 @@ Variant pick_spmm(int64_t L, bool al) {
 // plain SpMM of that width; any Lout.  Tiles of 16 rows per wave up to
 // Lin = 64, 12 at 128 and 4 above, so that LDS does not limit occupancy
 // (measured on MI355X, R-MAT 2^20 rows).
+//
+// For the fused form (<SDDMM, SpMM, GEMM>) at Lin <= 64, the dense matrix is
+// staged in LDS once per block (epi_wl) when it takes at most 64 KB, with
+// TRW rows per tile, and the block size is the one of 256, 512 or 1024
+// threads that gives the most waves per CU within the LDS of a CU (at most
+// 24, the register limit of these kernels; ties go to the larger block,
+// which copies the matrix fewer times).  Measured on MI355X, R-MAT 2^20 rows
+// at the paper's sizes: 2-3% faster for <SDDMM, SpMM, GEMM> (64 x 64, 512
+// threads, 24 waves per CU); 1.2-1.4x slower for the SpMM forms at Lin = 128
+// (64 KB or 32 KB staged leave 16 waves per CU) and 1.2x slower for
+// <SpMM, GEMM> at 64 x 64, so those read the matrix through the caches.
+constexpr size_t kLdsPerCu = 160 * 1024;
+constexpr int kEpiWavesCap = 24;
+
+template <int MODE, int W, int LV, int HAD, int TR, int TRW>
+Variant epi_best(int64_t Lout, size_t max_lds_block) {
+  constexpr int LIN = W * LV;
+  if constexpr (MODE == kFused && LIN <= 64) {
+    if ((int64_t)LIN * Lout * 4 > 65536) return epi<MODE, W, LV, HAD, TR>();
+    Variant best{};
+    int best_waves = 0;
+    for (int block : {1024, 512, 256}) {
+      Variant v = epi_wl<MODE, W, LV, HAD, TRW>(Lout, block);
+      if (v.lds > max_lds_block || v.lds > kLdsPerCu) continue;
+      int waves = (int)(kLdsPerCu / v.lds) * (block / 64);
+      if (waves > kEpiWavesCap) waves = kEpiWavesCap;
+      if (waves > best_waves) {
+        best = v;
+        best_waves = waves;
+      }
+    }
+    if (best.fn) return best;
+  }
+  return epi<MODE, W, LV, HAD, TR>();
+}
+
+bool epi_width(int64_t Lin) {
+  return Lin == 16 || Lin == 32 || Lin == 64 || Lin == 128 || Lin == 256 || Lin == 512;
+}
+
 template <int MODE, int HAD>
-Variant pick_epi(int64_t Lin) {
+Variant pick_epi(int64_t Lin, int64_t Lout, size_t max_lds_block) {
   switch (Lin) {
-    case 16: return epi<MODE, 4, 4, HAD, 16>();
-    case 32: return epi<MODE, 8, 4, HAD, 16>();
-    case 64: return epi<MODE, 16, 4, HAD, 16>();
-    case 128: return epi<MODE, 32, 4, HAD, 12>();
-    case 256: return epi<MODE, 64, 4, HAD, 4>();
-    case 512: return epi<MODE, 64, 8, HAD, 4>();
+    case 16: return epi_best<MODE, 4, 4, HAD, 16, 16>(Lout, max_lds_block);
+    case 32: return epi_best<MODE, 8, 4, HAD, 16, 16>(Lout, max_lds_block);
+    case 64: return epi_best<MODE, 16, 4, HAD, 16, 16>(Lout, max_lds_block);
+    case 128: return epi_best<MODE, 32, 4, HAD, 12, 8>(Lout, max_lds_block);
+    case 256: return epi_best<MODE, 64, 4, HAD, 4, 4>(Lout, max_lds_block);
+    case 512: return epi_best<MODE, 64, 8, HAD, 4, 4>(Lout, max_lds_block);
     default: return Variant{};
   }
 }
@@ -381,7 +455,7 @@ int blocks_per_cu(int dev, KernelFn fn, int block, size_t lds, int *out) {
     int unset = 0;
     g_grid_factor.compare_exchange_strong(unset, f >= 1 && f <= kMaxGridFactor ? f : -1);
   }
-  auto key = std::make_pair(dev, (uintptr_t)fn);
+  auto key = std::make_pair(dev, std::make_pair((uintptr_t)fn, lds));
   auto it = g_occupancy.find(key);
   if (it != g_occupancy.end()) {
     *out = it->second;
@@ -648,8 +722,14 @@ int run_epilogue(Mode mode, bool had, const int32_t *rowptr, const int32_t *coli
                  const float *vals, const float *C, const float *D, const float *E,
                  const float *G2, const float *Wm, float *A, int64_t N, int64_t Kdot,
                  int64_t Lin, int64_t Lout, void *stream) {
-  Variant v = mode == kFused ? pick_epi<kFused, 0>(Lin)
-                             : (had ? pick_epi<kSpmm, 1>(Lin) : pick_epi<kSpmm, 0>(Lin));
+  if (!epi_width(Lin)) return SPARSELNR_ERR_UNSUPPORTED;  // before any HIP call
+  int dev = 0, rc;
+  size_t max_lds = 0;
+  if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  if ((rc = device_max_lds(dev, &max_lds)) != SPARSELNR_OK) return rc;
+  Variant v = mode == kFused ? pick_epi<kFused, 0>(Lin, Lout, max_lds)
+                             : (had ? pick_epi<kSpmm, 1>(Lin, Lout, max_lds)
+                                    : pick_epi<kSpmm, 0>(Lin, Lout, max_lds));
   if (!v.fn) return SPARSELNR_ERR_UNSUPPORTED;
   WalkArgs a = base_args(rowptr, colidx, vals, N, Kdot, Lout);
   a.C = C;
@@ -829,8 +909,7 @@ int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx, const flo
   if (rc != SPARSELNR_OK) return rc;
   if (N == 0 || L == 0) return SPARSELNR_OK;
   if (!(aligned16(C) && aligned16(D) && offsets32(M, J))) return SPARSELNR_ERR_UNSUPPORTED;
-  Variant vs[2] = {pick_epi<kSpmm, 0>(J), pick_epi<kSpmm, 1>(J)};
-  if (!vs[0].fn || !vs[1].fn) return SPARSELNR_ERR_UNSUPPORTED;
+  if (!epi_width(J)) return SPARSELNR_ERR_UNSUPPORTED;
   if (M == 0 || J == 0)  // no rows to gather: the per-nonzero form alone
     return run_epilogue(kSpmm, true, rowptr, colidx, vals, nullptr, nullptr, C, D, E, A, N, 0, J,
                         L, stream);
@@ -840,7 +919,11 @@ int sparselnr_spmmh_gemm(const int32_t *rowptr, const int32_t *colidx, const flo
   // fewer bytes when nnz >= 3 M.  nnz is known on the device only, so both
   // schedules are launched, gated on it, and exactly one of them runs.
   int dev = 0;
+  size_t max_lds = 0;
   if ((rc = current_device(&dev)) != SPARSELNR_OK) return rc;
+  if ((rc = device_max_lds(dev, &max_lds)) != SPARSELNR_OK) return rc;
+  Variant vs[2] = {pick_epi<kSpmm, 0>(J, L, max_lds), pick_epi<kSpmm, 1>(J, L, max_lds)};
+  if (!vs[0].fn || !vs[1].fn) return SPARSELNR_ERR_UNSUPPORTED;
   hipStream_t s = (hipStream_t)stream;
   void *ws = nullptr;
   if ((rc = get_workspace(dev, s, (size_t)M * J * sizeof(float), &ws, 2)) != SPARSELNR_OK)
