@@ -665,6 +665,11 @@ def main() -> int:
         "data": "synthetic",
         "config": dict({"workload": wl["desc"], "kernel": args.kernel}, **wl["sizes"]),
         "roofline": roofline, "cpu_baseline": cpu, "parity": parity,
+        "counters": ({"kernel": traffic["dominant"],
+                      "l2_hit_rate": traffic.get("l2_hit_rate"),
+                      "valu_busy_pct": traffic.get("valu_busy_pct"),
+                      "source": "rocprofv3 --pmc passes committed under profiles/ (counters_%s.md)"
+                                % key} if traffic else None),
         "paper_context": dict(PAPER_CONTEXT[args.kernel], hardware=PAPER_HARDWARE,
                               use="context only: the paper's CPU speedups over TACO, not a "
                                   "target for this GPU path"),

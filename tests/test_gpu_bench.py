@@ -42,8 +42,13 @@ def test_bench_json_line(gpu):
         assert roof["traffic"] == stored["bytes_per_call"] > 0
         ms = d["ms_per_step"]
         assert abs(roof["traffic_frac"] - roof["traffic"] / (ms * 1e-3) / 8e12) < 1e-3
+        ctr = d["counters"]
+        assert ctr["kernel"] == stored["dominant"]
+        assert ctr["l2_hit_rate"] == stored.get("l2_hit_rate")
+        assert ctr["valu_busy_pct"] == stored.get("valu_busy_pct")
     else:
         assert roof["traffic"] is None and roof["traffic_frac"] is None
+        assert d["counters"] is None
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
     host = cpu["host"]
