@@ -38,7 +38,9 @@ def lengths(seed):
 
 
 @pytest.mark.parametrize("L,Mo", [(32, 32), (32, 16), (64, 64), (64, 32), (128, 128), (128, 64),
-                                  (16, 48), (256, 100), (512, 64), (64, 1)])
+                                  (16, 48), (256, 100), (512, 64), (64, 1),
+                                  # dense matrix staged in LDS with blocks above 64 KB of LDS
+                                  (64, 128), (64, 256), (32, 512), (16, 1024), (64, 257)])
 def test_sddmm_spmm_gemm(gpu, L, Mo):
     p = make_problem(lengths(L + Mo), 2000, L, L, seed=L, dense="normal")
     W = synth.normal(5, 9, (L, Mo))
