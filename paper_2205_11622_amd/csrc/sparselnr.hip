@@ -27,7 +27,7 @@ constexpr int kBlock = 256;       // threads per block (4 waves)
 // (uniform 65536 x 16: fused +1.5%, unfused -1.4%).  Smaller blocks leave the
 // dispatcher a finer-grained tail and spread each XCD's share more evenly.
 constexpr int kWalkBlock = 64;
-constexpr int kMinChunk = 64;     // smallest merge-path slice per worker
+constexpr int kMinChunk = 64;     // smallest merge-path slice per worker (see slice_count)
 constexpr int kXcds = 8;          // MI355X deals blocks over 8 XCDs
 constexpr int kGridFactor = 8;    // resident grids per walk launch for large inputs
 constexpr int kGenericLT = 4;     // generic path: 4 x 64 = 256 columns per tile
@@ -223,6 +223,12 @@ constexpr int kPU128 = 8;
 // nonzeros per paced step at K = L = 32 and 64 (measured on MI355X: 8 per step
 // is 8% faster on 65536 rows of 16 nonzeros, 4 is 1% faster on R-MAT 2^22).
 constexpr int kPUs = 8;
+// Gather schedule of the small-input fused kernel at K = L = 32: all gathers
+// of a step at once.  Measured on MI355X, 2048 rows of 10 nonzeros (16-item
+// slices): 12.3 us per call against 13.2 paced.  At K = L = 64 the burst
+// walk is 5% slower on 65536 rows of 16 nonzeros, which keep 64-item slices
+// and the paced walk.
+constexpr int kSmall32 = slnr::kBurst;
 
 // The 64-lane fused kernel of large inputs at K = L = 128 takes 10 nonzeros
 // per paced step (measured on MI355X, R-MAT 2^20: 1.5-2.3% faster than 8 on
@@ -333,7 +339,7 @@ Variant fused_fast_l(int64_t L) {
 Variant pick_fused(int64_t K, int64_t L, bool al) {
   if (al) {
     if (K == 32 && L == 32) return with_small(fast<kFused, 8, 1, 4, 4, kFS, kPU>(),
-                                              slnr::walk_fast<kFused, 8, 1, 4, 4, kFS, kPUs>);
+                                              slnr::walk_fast<kFused, 8, 1, 4, 4, kSmall32, kPUs>);
     if (K == 64 && L == 64)
       return with_wide<kFused, 1, 1, kFS, kPU>(with_small(
           fast<kFused, 16, 1, 4, 4, kFS, kPU>(), slnr::walk_fast<kFused, 16, 1, 4, 4, kFS, kPUs>));

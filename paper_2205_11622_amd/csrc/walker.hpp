@@ -44,7 +44,11 @@ enum Mode : int { kFused = 0, kSddmm = 1, kSpmm = 2 };
 //              row has arrived, then all arithmetic.  Fewer requests in
 //              flight per worker keeps workers of an XCD in step, which keeps
 //              rows shared by neighbouring rows (banded matrices) in L2.
-enum Sched : int { kPipelined = 0, kPaced = 1 };
+//  kBurst      all index broadcasts of the step, then all of its gathers at
+//              once, then all arithmetic: one memory latency per step.  For
+//              inputs too small to fill the GPU, whose time is the chain of
+//              dependent loads of one worker, not the traffic.
+enum Sched : int { kPipelined = 0, kPaced = 1, kBurst = 2 };
 
 // s_waitcnt immediate (gfx9 encoding) waiting for vmcnt <= V only.
 template <int V>
@@ -216,33 +220,52 @@ __device__ __forceinline__ T ld_stream(const T *p) {
 // ------------------------------------------------------------ merge path
 
 // Largest row i in [max(0, d - nnz), min(d, N)] with rowptr[i] + i <= d: the
-// merge-path coordinate (i row ends, d - i nonzeros consumed) of diagonal d.
-// rowptr[i] + i is strictly increasing in i.  The G lanes of a worker probe
-// G points of the current interval at once and keep the sub-interval the
-// ballot points to, so the search takes log_G(N) steps instead of log_2(N)
-// dependent loads.  All lanes of the group return the same value.
+// merge-path coordinate (i row ends, d - i nonzeros consumed) of diagonal d,
+// for the two diagonals da and db at once.  rowptr[i] + i is strictly
+// increasing in i.  The G lanes of a worker probe G points of each current
+// interval at once and keep the sub-interval the ballot points to, so a
+// search takes log_G(N) steps instead of log_2(N) dependent loads, and the
+// two searches share their steps (both probes of a step are loaded before
+// either ballot).  All lanes of the group return the same values.
 template <int G>
-__device__ __forceinline__ int64_t mp_search(const int32_t *rowptr, int64_t N, int64_t nnz,
-                                             int64_t d) {
+__device__ __forceinline__ void mp_search2(const int32_t *rowptr, int64_t N, int64_t nnz,
+                                           int64_t da, int64_t db, int64_t *ia, int64_t *ib) {
   const int lane = threadIdx.x & 63;
   const int glane = lane & (G - 1);
   const int gbase = lane - glane;
-  int64_t lo = d > nnz ? d - nnz : 0;  // rowptr[lo] + lo <= d always holds
-  int64_t hi = d < N ? d : N;
-  while (lo < hi) {
-    const int64_t step = (hi - lo + G - 1) / G;
-    int64_t x = lo + (int64_t)(glane + 1) * step;
-    if (x > hi) x = hi;
-    const bool ok = (int64_t)rowptr[x] + x <= d;
-    const uint64_t ball = __ballot(ok);
-    const uint64_t bits = G == 64 ? ball : (ball >> gbase) & ((1ull << (G & 63)) - 1);
-    const int m = (~bits == 0) ? 64 : __builtin_ctzll(~bits);  // probes 0..m-1 hold
-    const int64_t xm1 = lo + (int64_t)m * step;                 // probe m-1 (if m > 0)
-    const int64_t xm = lo + (int64_t)(m + 1) * step;            // probe m (if m < G)
-    if (m > 0) lo = xm1 < hi ? xm1 : hi;
-    if (m < G) hi = (xm < hi ? xm : hi) - 1;
+  const int64_t d[2] = {da, db};
+  int64_t lo[2], hi[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    lo[t] = d[t] > nnz ? d[t] - nnz : 0;  // rowptr[lo] + lo <= d always holds
+    hi[t] = d[t] < N ? d[t] : N;
   }
-  return lo;
+  while (lo[0] < hi[0] || lo[1] < hi[1]) {
+    int64_t step[2], x[2];
+    int32_t r[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {  // a finished search probes its own end, which is in range
+      step[t] = (hi[t] - lo[t] + G - 1) / G;
+      x[t] = lo[t] + (int64_t)(glane + 1) * step[t];
+      if (x[t] > hi[t]) x[t] = hi[t];
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) r[t] = rowptr[x[t]];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (lo[t] < hi[t]) {  // uniform in the group
+        const uint64_t ball = __ballot((int64_t)r[t] + x[t] <= d[t]);
+        const uint64_t bits = G == 64 ? ball : (ball >> gbase) & ((1ull << (G & 63)) - 1);
+        const int m = (~bits == 0) ? 64 : __builtin_ctzll(~bits);  // probes 0..m-1 hold
+        const int64_t xm1 = lo[t] + (int64_t)m * step[t];           // probe m-1 (if m > 0)
+        const int64_t xm = lo[t] + (int64_t)(m + 1) * step[t];      // probe m (if m < G)
+        if (m > 0) lo[t] = xm1 < hi[t] ? xm1 : hi[t];
+        if (m < G) hi[t] = (xm < hi[t] ? xm : hi[t]) - 1;
+      }
+    }
+  }
+  *ia = lo[0];
+  *ib = lo[1];
 }
 
 struct Slice {
@@ -252,8 +275,21 @@ struct Slice {
   bool active;
 };
 
+// Slice length of inputs too small to fill the GPU, and the row length that
+// slices shorter than 64 items still keep whole.
+constexpr int64_t kShortSlice = 16;
+constexpr int64_t kSnapRow = 16;
+
 // Slices are S = max(min_chunk, ceil(items / workers)) items long, so small
-// inputs use only the first ns = ceil(items / S) of them.  With the XCD
+// inputs use only the first ns = ceil(items / S) of them.  An input with
+// fewer than kShortSlice items per worker cannot fill the GPU however it is
+// cut: its time is one worker's chain of dependent loads, so its slices are
+// kShortSlice items (about one short row and its end) and it spreads over
+// as many workers as it has such rows.  Measured on MI355X, 2048 rows of 10
+// nonzeros at K = L = 32: fused 22.6 -> 13.2 us per call, unfused 32.8 ->
+// 19.2 us, results bit-identical (no row is split either way); inputs with
+// 16 to 64 items per worker keep 64-item slices (65536 rows of 16 nonzeros:
+// the unfused passes 1.7% slower with 34-item slices).  With the XCD
 // remap, XCD x (blocks are dealt round-robin over the XCDs) takes the
 // contiguous run of slices [x * ns / xcds, (x + 1) * ns / xcds), so that the
 // workers sharing an L2 walk neighbouring rows and every XCD gets an equal
@@ -263,7 +299,8 @@ __device__ __forceinline__ void slice_count(const WalkArgs &a, int64_t *S_out, i
   const int64_t nnz = a.rowptr[a.N];
   const int64_t items = a.N + nnz;
   int64_t S = (items + a.workers - 1) / a.workers;
-  if (S < a.min_chunk) S = a.min_chunk;
+  if (S < kShortSlice) S = kShortSlice;
+  else if (S < a.min_chunk) S = a.min_chunk;
   *S_out = S;
   *ns_out = (items + S - 1) / S;
   *items_out = items;
@@ -293,15 +330,18 @@ __device__ __forceinline__ Slice make_slice(const WalkArgs &a) {
   if (!s.active) return s;
   const int64_t d0 = s.id * S;
   const int64_t d1 = d0 + S < items ? d0 + S : items;
-  s.i0 = mp_search<W>(a.rowptr, a.N, nnz, d0);
+  mp_search2<W>(a.rowptr, a.N, nnz, d0, d1, &s.i0, &s.i1);
   s.p0 = d0 - s.i0;
-  s.i1 = mp_search<W>(a.rowptr, a.N, nnz, d1);
   s.p1 = d1 - s.i1;
-  // A boundary inside a short row (at most S/4 nonzeros) moves back to the
-  // row's start, so only long rows are ever split between slices.  Both
-  // slices sharing the boundary apply the same rule, and the rule is
-  // monotone, so slices stay contiguous and ordered.
-  const int64_t snap = S / 4;
+  // A boundary inside a short row moves back to the row's start, so only
+  // long rows are ever split between slices.  Short means at most S/4
+  // nonzeros for slices of 64 items or more; the shorter slices of small
+  // inputs keep rows of up to min(S, 16) nonzeros whole, so that such inputs
+  // leave no partial rows to the fixup.  Both slices sharing the boundary
+  // apply the same rule, and the rule is monotone, so slices stay contiguous
+  // and ordered; snap never exceeds S, so no slice is left empty by it.
+  const int64_t snap_short = S < kSnapRow ? S : kSnapRow;
+  const int64_t snap = S / 4 > snap_short ? S / 4 : snap_short;
   auto snap_back = [&](int64_t i, int64_t &p) {
     if (i < a.N) {
       const int64_t r0 = a.rowptr[i];
@@ -330,7 +370,7 @@ struct Gather {
 // NB  nonzeros per producer pass; PS = W / NB lanes form one dot product.
 // KV  floats of C_i / D_j per producer lane (K = PS * KV).
 // LV  floats of E_j / A_i per lane (L = W * LV).
-// SCHED, U  gather schedule and, for kPaced, the nonzeros per step.
+// SCHED, U  gather schedule and, for kPaced and kBurst, the nonzeros per step.
 // HAD  the consumer row is E_j .* G2_j (Hadamard product of two gathers).
 //
 // The state is group-uniform (all W lanes agree on p, n), so lane-group
@@ -354,6 +394,8 @@ struct RowWalk {
   static_assert(W >= 4 && W <= 64 && (W & (W - 1)) == 0, "W");
   static_assert(NB >= 1 && W % NB == 0, "NB");
   static_assert(SCHED == kPipelined || (U >= 1 && U <= W && (NB == 1 || U == NB)), "U");
+  static_assert(SCHED != kBurst || NB == 1, "burst steps are built for one dot per pass");
+  static constexpr bool kStep = SCHED == kPaced || SCHED == kBurst;
   static_assert(!HAD || (NB == 1 && MODE == kSpmm), "Hadamard rows come with the one-dot SpMM");
 
   const int32_t *__restrict__ colidx;
@@ -406,9 +448,9 @@ struct RowWalk {
         // producer pass of the multi-dot variant)
         int n = (int)(r_end - p < wb + W - p ? r_end - p : wb + W - p);
         if (NB > 1 && n > NB) n = NB;
-        if (SCHED == kPaced && n > U) n = U;
+        if (kStep && n > U) n = U;
         const int off = (int)(p - wb);
-        if constexpr (NB == 1 && SCHED == kPaced) {
+        if constexpr (NB == 1 && kStep) {
           uint32_t jj[U];
           float bb[U];
   #pragma unroll
@@ -423,7 +465,7 @@ struct RowWalk {
   #pragma unroll
           for (int u = 0; u < U; ++u) {
             if (u < n) {
-              if (u > 0) wait_vmcnt<paced_in_flight<W, KV, LV>()>();
+              if (SCHED == kPaced && u > 0) wait_vmcnt<paced_in_flight<W, KV, LV>()>();
               if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
               if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
               if constexpr (HAD) ldv_off<LV>(hr[u], Gm, jj[u] * strideE + offE);

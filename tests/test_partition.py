@@ -33,13 +33,32 @@ def slice_bounds(rowptr, N, nnz, S, d, snap):
     return i, p
 
 
-def simulate(rowptr, workers, min_chunk, L=3, rng=None, use_snap=True):
+SHORT_SLICE = 16  # kShortSlice of the kernels
+SNAP_ROW = 16     # kSnapRow of the kernels
+
+
+def slice_len(items, workers, min_chunk, short=SHORT_SLICE):
+    """The kernels' slice length: ceil(items / workers), raised to `short`
+    below it and to min_chunk between the two."""
+    S = -(-items // workers)
+    if S < short:
+        return short
+    return max(S, min_chunk)
+
+
+def snap_len(S, snap_row=SNAP_ROW):
+    """Longest row a slice boundary never splits: S/4, or min(S, snap_row)
+    when that is larger (short slices)."""
+    return max(S // 4, min(S, snap_row))
+
+
+def simulate(rowptr, workers, min_chunk, L=3, rng=None, use_snap=True, short=SHORT_SLICE):
     """Returns (A, writes) computed through the slice / carry / fixup rules."""
     N = rowptr.size - 1
     nnz = int(rowptr[N])
     items = N + nnz
-    S = max(-(-items // workers), min_chunk)
-    snap = S // 4 if use_snap else -1
+    S = slice_len(items, workers, min_chunk, short)
+    snap = snap_len(S) if use_snap else -1
     rng = rng or np.random.default_rng(0)
     contrib = rng.integers(-5, 6, size=(nnz, L)).astype(np.float64)  # y_p * E_j, exact ints
     A = np.full((N, L), np.nan)
@@ -121,28 +140,57 @@ CASES = {
 }
 
 
+@pytest.mark.parametrize("short", [1, SHORT_SLICE])
 @pytest.mark.parametrize("use_snap", [True, False])
 @pytest.mark.parametrize("name", sorted(CASES))
 @pytest.mark.parametrize("workers,min_chunk", [(1, 1), (3, 1), (7, 2), (64, 1), (64, 32),
-                                                (1000, 1), (5, 1000), (40, 8)])
-def test_every_row_once(name, workers, min_chunk, use_snap):
+                                                (1000, 1), (5, 1000), (40, 8), (1000, 64)])
+def test_every_row_once(name, workers, min_chunk, use_snap, short):
     rowptr = csr_from_lengths(CASES[name])
-    A, writes, consumed, ref = simulate(rowptr, workers, min_chunk, use_snap=use_snap)
+    A, writes, consumed, ref = simulate(rowptr, workers, min_chunk, use_snap=use_snap,
+                                        short=short)
     assert np.all(consumed == 1)
     assert np.all(writes == 1)
     assert np.array_equal(A, ref)
 
 
-def test_snapping_splits_only_long_rows():
+def test_slice_length_rule():
+    # fewer than 16 items per worker: 16-item slices; 16 to 64: 64; above: the quotient
+    assert slice_len(22528, 32768, 64) == 16      # 2048 rows of 10 nonzeros
+    assert slice_len(1114112, 32768, 64) == 64    # 65536 rows of 16 nonzeros, 34 per worker
+    assert slice_len(1114112, 16384, 64) == 68
+    assert slice_len(15 * 100, 100, 64) == 16
+    assert slice_len(16 * 100, 100, 64) == 64
+    assert [snap_len(S) for S in (1, 7, 16, 63, 64, 68, 1000)] == [1, 7, 16, 16, 16, 17, 250]
+
+
+@pytest.mark.parametrize("workers", [300, 3000, 30000])
+def test_snapping_splits_only_long_rows(workers):
     lengths = [int(x) for x in (np.random.default_rng(2).pareto(1.2, 2000) * 3)]
     rowptr = csr_from_lengths(lengths)
     N, nnz = len(lengths), int(rowptr[-1])
-    workers = 300
-    S = max(-(-(N + nnz) // workers), 1)
-    for w in range(1, workers):
-        i, p = slice_bounds(rowptr, N, nnz, S, w * S, S // 4)
+    S = slice_len(N + nnz, workers, 64)
+    snap = snap_len(S)
+    assert snap <= S
+    for w in range(1, -(-(N + nnz) // S)):
+        i, p = slice_bounds(rowptr, N, nnz, S, w * S, snap)
         if i < N and p > rowptr[i]:
-            assert rowptr[i + 1] - rowptr[i] > S // 4
+            assert rowptr[i + 1] - rowptr[i] > snap
+
+
+def test_short_slices_keep_short_rows_whole():
+    # 2048 rows of 10 nonzeros on 32768 workers: 16-item slices, no partial rows
+    rowptr = csr_from_lengths([10] * 2048)
+    N, nnz = 2048, int(rowptr[-1])
+    S = slice_len(N + nnz, 32768, 64)
+    assert S == 16
+    ns = -(-(N + nnz) // S)
+    prev = (0, 0)
+    for w in range(1, ns + 1):
+        i, p = slice_bounds(rowptr, N, nnz, S, min(w * S, N + nnz), snap_len(S))
+        assert p == rowptr[i]  # every boundary at a row start
+        assert (i, p) > prev or (i, p) == (N, nnz)  # no empty slice
+        prev = (i, p)
 
 
 def test_rows_ending_on_slice_boundaries():
@@ -153,8 +201,16 @@ def test_rows_ending_on_slice_boundaries():
         items = len(lengths) + rowptr[-1]
         workers = -(-items // S)
         for use_snap in (True, False):
-            A, writes, consumed, ref = simulate(rowptr, workers, 1, use_snap=use_snap)
+            A, writes, consumed, ref = simulate(rowptr, workers, 1, use_snap=use_snap, short=1)
             assert np.all(consumed == 1) and np.all(writes == 1) and np.array_equal(A, ref)
+
+
+def mp_search2_wide(rowptr, N, nnz, da, db, G):
+    """Host model of the kernels' paired search: both diagonals advance in
+    the same steps, each by the rule of mp_search_wide."""
+    ra, sa = mp_search_wide(rowptr, N, nnz, da, G)
+    rb, sb = mp_search_wide(rowptr, N, nnz, db, G)
+    return ra, rb, max(sa, sb)
 
 
 def mp_search_wide(rowptr, N, nnz, d, G):
@@ -188,6 +244,18 @@ def test_wide_search_matches_bisection(G, name):
         got, steps = mp_search_wide(rowptr, N, nnz, d, G)
         assert got == mp_search(rowptr, N, nnz, d), (d, G)
         assert rowptr[got] <= d - got <= (rowptr[got + 1] if got < N else nnz)
+
+
+@pytest.mark.parametrize("G", [4, 8, 64])
+def test_paired_search_matches_two_searches(G):
+    rowptr = csr_from_lengths(CASES["power_law"])
+    N, nnz = rowptr.size - 1, int(rowptr[-1])
+    for S in (1, 7, 16, 64):
+        for d0 in range(0, N + nnz + 1, S):
+            d1 = min(d0 + S, N + nnz)
+            a, b, steps = mp_search2_wide(rowptr, N, nnz, d0, d1, G)
+            assert (a, b) == (mp_search(rowptr, N, nnz, d0), mp_search(rowptr, N, nnz, d1))
+            assert a <= b
 
 
 def test_wide_search_step_count():
