@@ -283,13 +283,17 @@ constexpr int64_t kSnapRow = 16;
 // Slices are S = max(min_chunk, ceil(items / workers)) items long, so small
 // inputs use only the first ns = ceil(items / S) of them.  An input with
 // fewer than kShortSlice items per worker cannot fill the GPU however it is
-// cut: its time is one worker's chain of dependent loads, so its slices are
-// kShortSlice items (about one short row and its end) and it spreads over
-// as many workers as it has such rows.  Measured on MI355X, 2048 rows of 10
-// nonzeros at K = L = 32: fused 22.6 -> 13.2 us per call, unfused 32.8 ->
-// 19.2 us, results bit-identical (no row is split either way); inputs with
-// 16 to 64 items per worker keep 64-item slices (65536 rows of 16 nonzeros:
-// the unfused passes 1.7% slower with 34-item slices).  With the XCD
+// cut: its time is one worker's chain of dependent loads.  If its rows
+// average at most kSnapRow nonzeros, its slices are kShortSlice items (about
+// one short row and its end), so it spreads over as many workers as it has
+// rows.  Measured on MI355X, 2048 rows of 10 nonzeros at K = L = 32: fused
+// 22.6 -> 13.2 us per call, unfused 32.8 -> 19.2 us, results bit-identical
+// (no row is split either way).  Inputs with longer rows on average keep
+// 64-item slices: a hub row there would split into 4x more partial rows,
+// which one wave of the fixup sums (1000 rows with one of 10^5 nonzeros:
+// 172 us against 90 at K = L = 32).  Inputs with 16 to 64 items per worker
+// also keep 64-item slices (65536 rows of 16 nonzeros: the unfused passes
+// 1.7% slower with 34-item slices).  With the XCD
 // remap, XCD x (blocks are dealt round-robin over the XCDs) takes the
 // contiguous run of slices [x * ns / xcds, (x + 1) * ns / xcds), so that the
 // workers sharing an L2 walk neighbouring rows and every XCD gets an equal
@@ -299,7 +303,7 @@ __device__ __forceinline__ void slice_count(const WalkArgs &a, int64_t *S_out, i
   const int64_t nnz = a.rowptr[a.N];
   const int64_t items = a.N + nnz;
   int64_t S = (items + a.workers - 1) / a.workers;
-  if (S < kShortSlice) S = kShortSlice;
+  if (S < kShortSlice && nnz <= kSnapRow * a.N) S = kShortSlice;
   else if (S < a.min_chunk) S = a.min_chunk;
   *S_out = S;
   *ns_out = (items + S - 1) / S;

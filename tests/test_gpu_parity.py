@@ -280,6 +280,37 @@ def test_deterministic_bit_exact(gpu):
     assert bool(torch_equal(Y1, Y2)) and bool(torch_equal(Au1, Au2))
 
 
+@pytest.mark.parametrize("K,L,factors", [(32, 32, (1, 2, 7, 64)), (64, 64, (2, 7, 64))])
+def test_short_rows_of_small_inputs_are_never_split(gpu, K, L, factors):
+    """An input with fewer than 16 merge-path items per worker takes 16-item
+    slices, and no slice boundary splits a row of at most 16 nonzeros: every
+    row is summed by one worker in nonzero order whatever the grid factor, so
+    the factors that launch the same lane mapping give bit-identical A (and
+    every factor matches the oracle).  At K = L = 32 every factor keeps the
+    8-lane mapping (the burst walk at one resident grid, the paced one
+    above); at K = L = 64 one resident grid takes 16-lane workers and more
+    take 64-lane ones."""
+    rng = np.random.default_rng(41 + K)
+    lengths = rng.integers(0, 17, size=3000)
+    p = make_problem(lengths, 2500, K, L, seed=43 + K)
+    d = upload(p)
+    ref = None
+    try:
+        for f in (1,) + tuple(factors):
+            slnr.sparselnr_set_grid_factor(f)
+            A = fused(d).clone()
+            check_A_rows(p, A, what="fused A, grid factor %d" % f)
+            Y, Au = unfused(d)
+            check_A_rows(p, Au, what="unfused A, grid factor %d" % f)
+            if f in factors:
+                if ref is None:
+                    ref = (A, Au.clone())
+                assert bool(torch_equal(A, ref[0])), "fused A differs at grid factor %d" % f
+                assert bool(torch_equal(Au, ref[1])), "unfused A differs at grid factor %d" % f
+    finally:
+        slnr.sparselnr_set_grid_factor(0)
+
+
 def torch_equal(a, b):
     import torch
     return torch.equal(a.view(torch.int32), b.view(torch.int32))

@@ -37,11 +37,13 @@ SHORT_SLICE = 16  # kShortSlice of the kernels
 SNAP_ROW = 16     # kSnapRow of the kernels
 
 
-def slice_len(items, workers, min_chunk, short=SHORT_SLICE):
+def slice_len(items, workers, min_chunk, short=SHORT_SLICE, N=None, nnz=None):
     """The kernels' slice length: ceil(items / workers), raised to `short`
-    below it and to min_chunk between the two."""
+    below it when the rows average at most SNAP_ROW nonzeros (N, nnz; None:
+    they do), else to min_chunk."""
     S = -(-items // workers)
-    if S < short:
+    short_rows = N is None or nnz <= SNAP_ROW * N
+    if S < short and short_rows:
         return short
     return max(S, min_chunk)
 
@@ -57,7 +59,7 @@ def simulate(rowptr, workers, min_chunk, L=3, rng=None, use_snap=True, short=SHO
     N = rowptr.size - 1
     nnz = int(rowptr[N])
     items = N + nnz
-    S = slice_len(items, workers, min_chunk, short)
+    S = slice_len(items, workers, min_chunk, short, N, nnz)
     snap = snap_len(S) if use_snap else -1
     rng = rng or np.random.default_rng(0)
     contrib = rng.integers(-5, 6, size=(nnz, L)).astype(np.float64)  # y_p * E_j, exact ints
@@ -161,6 +163,11 @@ def test_slice_length_rule():
     assert slice_len(1114112, 16384, 64) == 68
     assert slice_len(15 * 100, 100, 64) == 16
     assert slice_len(16 * 100, 100, 64) == 64
+    # rows averaging more than 16 nonzeros (a hub row) keep 64-item slices
+    assert slice_len(22528, 32768, 64, N=2048, nnz=20480) == 16
+    assert slice_len(2048 + 32768, 32768, 64, N=2048, nnz=32768) == 16
+    assert slice_len(2048 + 32769, 32768, 64, N=2048, nnz=32769) == 64
+    assert slice_len(1000 + 108000, 32768, 64, N=1000, nnz=108000) == 64
     assert [snap_len(S) for S in (1, 7, 16, 63, 64, 68, 1000)] == [1, 7, 16, 16, 16, 17, 250]
 
 
@@ -169,7 +176,7 @@ def test_snapping_splits_only_long_rows(workers):
     lengths = [int(x) for x in (np.random.default_rng(2).pareto(1.2, 2000) * 3)]
     rowptr = csr_from_lengths(lengths)
     N, nnz = len(lengths), int(rowptr[-1])
-    S = slice_len(N + nnz, workers, 64)
+    S = slice_len(N + nnz, workers, 64, N=N, nnz=nnz)
     snap = snap_len(S)
     assert snap <= S
     for w in range(1, -(-(N + nnz) // S)):
@@ -182,7 +189,7 @@ def test_short_slices_keep_short_rows_whole():
     # 2048 rows of 10 nonzeros on 32768 workers: 16-item slices, no partial rows
     rowptr = csr_from_lengths([10] * 2048)
     N, nnz = 2048, int(rowptr[-1])
-    S = slice_len(N + nnz, 32768, 64)
+    S = slice_len(N + nnz, 32768, 64, N=N, nnz=nnz)
     assert S == 16
     ns = -(-(N + nnz) // S)
     prev = (0, 0)
