@@ -388,10 +388,16 @@ Variant pick_spmm(int64_t L, bool al) {
 }
 
 // Section 6.2 benchmarks with a per-row epilogue.  Lin (the width of the
-// gathered rows and of t_i) in {16, 32, 64, 128, 256, 512}, walked like the
-// plain SpMM of that width; any Lout.  Tiles of 16 rows per wave up to
-// Lin = 64, 12 at 128 and 4 above, so that LDS does not limit occupancy
-// (measured on MI355X, R-MAT 2^20 rows).
+// gathered rows and of t_i) in {16, 32, 64, 128, 256, 512}; any Lout.
+// Workers of Lin / 4 lanes (4 floats per lane) from Lin = 64 on, of 16 lanes
+// below: 4- and 8-lane workers put 16 and 8 workers in a wave, so a 16-row
+// tile fills every round or two and is multiplied nearly empty, and the
+// shorter slices of the extra workers split more rows, whose partial rows
+// are Lout wide (measured on MI355X, R-MAT 2^20, <SpMM, GEMM>: 16 x 512
+// 2.03 against 2.79 ms, 16 x 256 1.38 against 1.71, 32 x 512 2.25 against
+// 2.52, 32 x 128 1.06 against 1.09; within 1% at Lout <= 64).  Tiles of 16
+// rows per wave up to Lin = 64, 12 at 128 and 4 above, so that LDS does not
+// limit occupancy (measured on MI355X, R-MAT 2^20 rows).
 //
 // For the fused form (<SDDMM, SpMM, GEMM>) at Lin <= 64, the dense matrix is
 // staged in LDS once per block (epi_wl) when it takes at most 64 KB, with
@@ -435,8 +441,8 @@ bool epi_width(int64_t Lin) {
 template <int MODE, int HAD>
 Variant pick_epi(int64_t Lin, int64_t Lout, size_t max_lds_block) {
   switch (Lin) {
-    case 16: return epi_best<MODE, 4, 4, HAD, 16, 16>(Lout, max_lds_block);
-    case 32: return epi_best<MODE, 8, 4, HAD, 16, 16>(Lout, max_lds_block);
+    case 16: return epi_best<MODE, 16, 1, HAD, 16, 16>(Lout, max_lds_block);
+    case 32: return epi_best<MODE, 16, 2, HAD, 16, 16>(Lout, max_lds_block);
     case 64: return epi_best<MODE, 16, 4, HAD, 16, 16>(Lout, max_lds_block);
     case 128: return epi_best<MODE, 32, 4, HAD, 12, 8>(Lout, max_lds_block);
     case 256: return epi_best<MODE, 64, 4, HAD, 4, 4>(Lout, max_lds_block);
