@@ -57,6 +57,8 @@ CPU_SECONDS = 10.0  # oracle passes are repeated until about this much wall time
 # at their own fastest one.
 GRID_FACTORS = (1, 2, 4, 8, 12, 16, 24, 32, 48, 64)
 TUNE_CALLS = 5
+# Untimed, waited-for calls before each timed region, in seconds of wall time.
+SETTLE_S = 0.05
 SMALL_CONFIGS = ("tiny", "uniform")  # calls of tens of microseconds: more timed calls by default
 SMALL_STEPS = 200
 
@@ -538,9 +540,21 @@ def main() -> int:
                 fn()
         return run
 
+    def settle(fn, seconds=SETTLE_S):
+        """Untimed calls, each waited for, until `seconds` of wall time have
+        passed: a call of a few microseconds otherwise meets the GPU still at
+        the clocks of the host-side set-up before it."""
+        t_end = time.perf_counter() + seconds
+        while True:
+            fn()
+            torch.cuda.synchronize()
+            if time.perf_counter() >= t_end:
+                break
+
     call_parts = [("timed call", wl["call"])]
     call_factors, call_tuning = factors_for(call_parts, args.grid_factor, "--grid-factor")
     call = bound(call_parts, call_factors)
+    settle(call)
     per, total_ms, wall = timed(call, args.steps, args.warmup)
     ms = total_ms / args.steps
     print("# fused: %.4f ms/call (median %.4f, min %.4f, max %.4f)"
@@ -551,6 +565,7 @@ def main() -> int:
         parts = wl["compare_parts"]
         cmp_factors, cmp_tuning = factors_for(parts, args.compare_grid_factor,
                                               "--compare-grid-factor")
+        settle(bound(parts, cmp_factors))
         uper, utotal, _ = timed(bound(parts, cmp_factors), args.steps, args.warmup)
         # interleave a second fused round so both see the same machine state
         per2, total2, _ = timed(call, args.steps, 1)
