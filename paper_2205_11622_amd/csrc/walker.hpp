@@ -27,6 +27,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace slnr {
 
 // Streams read or written once per call carry the nontemporal hint (C, the
@@ -280,8 +282,9 @@ struct Slice {
 constexpr int64_t kShortSlice = 16;
 constexpr int64_t kSnapRow = 16;
 
-// Slices are S = max(min_chunk, ceil(items / workers)) items long, so small
-// inputs use only the first ns = ceil(items / S) of them.  An input with
+// Slices are S = ceil(items / workers) items long, raised to min_chunk (or
+// to kShortSlice, below), so small inputs use only the first
+// ns = ceil(items / S) of them.  An input with
 // fewer than kShortSlice items per worker cannot fill the GPU however it is
 // cut: its time is one worker's chain of dependent loads.  If its rows
 // average at most kSnapRow nonzeros, its slices are kShortSlice items (about
@@ -814,38 +817,57 @@ __device__ __forceinline__ int64_t tail_run_start(const int32_t *__restrict__ me
   return first;
 }
 
-// Lanes over columns, partials summed in slice order.  The loads of a batch
-// are issued together, so a row split over hundreds of slices (a power-law
-// hub row) costs a few memory latencies rather than one per slice.
-__device__ __forceinline__ void fix_row(const WalkArgs &a, int64_t c, int32_t r) {
-  const float *__restrict__ carry = a.carry;
-  float *__restrict__ A = a.out;
-  const int64_t Lw = a.Lw, L = a.L, l0 = a.l0;
+// Partials first .. c-1 (tail slots) and c (head slot) of one row summed in
+// slice order, V consecutive columns per lane (V = 4: one 16-byte load per
+// partial, so a row of Lw columns takes Lw / 256 passes instead of Lw / 64;
+// each column's sum is taken in the same order either way, so the results
+// are bit-identical).  The loads of a batch are issued together, so a row
+// split over hundreds of slices (a power-law hub row) costs a few memory
+// latencies rather than one per slice.
+template <int V>
+__device__ __forceinline__ void fix_cols(const float *__restrict__ carry, float *__restrict__ arow,
+                                         int64_t Lw, int64_t first, int64_t c) {
+  typedef typename std::conditional<V == 4, f4_t, float>::type vec;
+  constexpr int kBatch = V == 4 ? 4 : 16;
   const int lane = threadIdx.x & 63;
-  const int64_t first = tail_run_start(a.meta, c, r);
-  constexpr int kBatch = 16;
-  for (int64_t l = lane; l < Lw; l += 64) {
-    float sum = 0.f;
+  auto at = [&](int64_t slot, int64_t l) {
+    return *reinterpret_cast<const vec *>(carry + slot * Lw + l);
+  };
+  for (int64_t l = (int64_t)V * lane; l < Lw; l += 64 * V) {
+    vec sum = vec{};
     int64_t cc = first;
     for (; cc + kBatch <= c; cc += kBatch) {
-      float v[kBatch];
+      vec v[kBatch];
 #pragma unroll
-      for (int t = 0; t < kBatch; ++t) v[t] = carry[((cc + t) * 2 + 1) * Lw + l];
+      for (int t = 0; t < kBatch; ++t) v[t] = at((cc + t) * 2 + 1, l);
 #pragma unroll
       for (int t = 0; t < kBatch; ++t) sum += v[t];
     }
     if (cc < c) {
-      float v[kBatch];
+      vec v[kBatch];
 #pragma unroll
       for (int t = 0; t < kBatch; ++t)
-        if (cc + t < c) v[t] = carry[((cc + t) * 2 + 1) * Lw + l];
+        if (cc + t < c) v[t] = at((cc + t) * 2 + 1, l);
 #pragma unroll
       for (int t = 0; t < kBatch; ++t)
         if (cc + t < c) sum += v[t];
     }
-    sum += carry[(c * 2) * Lw + l];
-    A[(int64_t)r * L + l0 + l] = sum;
+    sum += at(c * 2, l);
+    *reinterpret_cast<vec *>(arow + l) = sum;
   }
+}
+
+// Row r of A from its partials: 16-byte pieces when the widths and the
+// addresses allow them (uniform over the grid), single floats otherwise.
+__device__ __forceinline__ void fix_row(const WalkArgs &a, int64_t c, int32_t r) {
+  const int64_t Lw = a.Lw;
+  const int64_t first = tail_run_start(a.meta, c, r);
+  float *const arow = a.out + (int64_t)r * a.L + a.l0;
+  const bool v4 = (Lw & 3) == 0 && (a.L & 3) == 0 && (a.l0 & 3) == 0 &&
+                  (reinterpret_cast<uintptr_t>(a.out) & 15) == 0 &&
+                  (reinterpret_cast<uintptr_t>(a.carry) & 15) == 0;
+  if (v4) fix_cols<4>(a.carry, arow, Lw, first, c);
+  else fix_cols<1>(a.carry, arow, Lw, first, c);
 }
 
 __global__ __launch_bounds__(256) void carry_fixup(WalkArgs a, int G) {
