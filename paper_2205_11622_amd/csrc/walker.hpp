@@ -384,16 +384,12 @@ struct Gather {
 // divergence inside a wave only masks whole groups.  The colidx / vals window
 // (one entry per lane) keeps the dependent loads off the critical path; the
 // gathered D_j and E_j rows are plain loads so the hot columns stay in L2.
-// Gathers a paced step lets stay in flight when it issues its next nonzero:
-// one, except for the 64-lane worker with one float of each row per lane
-// (K = L = 64, large inputs), which takes two.  Measured on MI355X, R-MAT
-// 2^22: 1.5-2.3% faster than one at 16-64 resident grids, bit-identical;
-// three and no wait at all are within 0.5% of two.  The wider rows of rmat1m
-// and the stencil run slower with more than one.
-template <int W, int KV, int LV>
-constexpr int paced_in_flight() {
-  return W == 64 && KV == 1 && LV == 1 ? 2 : 1;
-}
+// A paced step issues a nonzero's gathers once every load of the previous
+// nonzero but the newest has arrived (vmcnt <= 1).  Letting two stay in
+// flight measured 9-10% slower on MI355X for the 64-lane worker with one
+// float of each row per lane (R-MAT 2^22, K = L = 64, three boxes, builds
+// compared in one process), and slower for the wider rows of rmat1m and
+// the stencil.
 
 template <int MODE, int W, int NB, int KV, int LV, int SCHED, int U, int HAD = 0>
 struct RowWalk {
@@ -472,7 +468,7 @@ struct RowWalk {
   #pragma unroll
           for (int u = 0; u < U; ++u) {
             if (u < n) {
-              if (SCHED == kPaced && u > 0) wait_vmcnt<paced_in_flight<W, KV, LV>()>();
+              if (SCHED == kPaced && u > 0) wait_vmcnt<1>();
               if constexpr (MODE != kSpmm) ldv_off<KV>(dr[u], Dm, jj[u] * strideD + offD);
               if constexpr (MODE != kSddmm) ldv_off<LV>(er[u], Em, jj[u] * strideE + offE);
               if constexpr (HAD) ldv_off<LV>(hr[u], Gm, jj[u] * strideE + offE);
